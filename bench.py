@@ -1,0 +1,202 @@
+#!/usr/bin/env python3
+"""Tree-verification throughput on one MI355X.
+
+One step = one pass of the whole hot path (tree-masked attention + residual,
+LM head, fused vocab pass with strict/relaxed acceptance, path reduction)
+over one batch of synthetic input, through the C ABI.  Default workload: the
+7B-shaped verify (hidden 4096, 32/32 heads, head_dim 128, vocab 32000, KV
+length 2048, a 26-node random draft tree, bf16 with fp32 accumulation).
+
+Inputs are resident in HBM before timing starts.  Several copies of the large
+inputs (K/V cache, LM head, hidden states) are rotated from step to step so
+that the working set exceeds the 256 MB Infinity Cache and every step streams
+its bytes from HBM.  Per-stage HIP events are recorded on the step's stream
+inside the timed region; they give each kernel's average duration for the
+roofline figures.  The CPU baseline times the oracle on the host cores on a
+bounded sample of the same workload.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0    # dense MFMA bf16
+FP32_PEAK_TFLOPS = 157.3
+MALL_BYTES = 256 << 20
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def stage_bytes(w, M, es):
+    """Algorithmic HBM bytes per launch of each stage (inputs read once, outputs written once)."""
+    s = w.shape
+    kv_rows = sum(int(w.kv_len[b]) + int(w.node_off[b + 1] - w.node_off[b]) for b in range(len(w.kv_len)))
+    attn = 2 * s.n_kv_heads * kv_rows * s.head_dim * es + 2 * M * s.hidden * es   # K,V + h in + x out
+    lm = s.vocab * s.hidden * es + M * s.hidden * es + M * s.vocab * 4            # W + x + logits out
+    vocab = M * s.vocab * 4                                                        # logits read once
+    vis = 0
+    for b in range(len(w.kv_len)):
+        lo, hi = int(w.node_off[b]), int(w.node_off[b + 1])
+        depth = [0] * (hi - lo)
+        for j in range(1, hi - lo):
+            depth[j] = depth[int(w.parent[lo + j])] + 1
+        vis += sum(int(w.kv_len[b]) + d + 1 for d in depth)
+    attn_flops = 4 * s.n_q_heads * s.head_dim * vis                                # QK^T + PV
+    lm_flops = 2 * M * s.vocab * s.hidden
+    return dict(attn=attn, lm=lm, vocab=vocab, attn_flops=attn_flops, lm_flops=lm_flops)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=1, help="workload shape (default: 7B-shaped 26-node verify)")
+    ap.add_argument("--rotate", type=int, default=0, help="input copies rotated per step (0: enough to exceed MALL)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the CPU oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the verification step of one tree runs on one device).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import respec_synth as synth
+    from paper_2511_01282_amd import binding, runner
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = args.config
+    shp = synth.CONFIGS[cfg]
+    es = 2 if shp.dtype == "bf16" else 4
+    log(f"[bench] generating workload {cfg} ({shp.name})")
+    w = synth.generate(cfg)
+    M = int(w.node_off[-1])
+    B = len(w.kv_len)
+
+    plan = runner.make_plan(w, dev)
+    base = runner.upload(w, dev)
+    kw = runner.step_kwargs(w)
+    out = binding.alloc_outputs(total_nodes=M, batch=B, hidden=shp.hidden, vocab=shp.vocab,
+                                topk_out=shp.topk_out, max_depth=shp.max_depth, device=dev, attn_out=False)
+
+    # draft tokens: the workload's argmax-prefix rule, using the GPU's own argmax
+    plan.step(base, out, **kw)
+    torch.cuda.synchronize()
+    argmax = out["argmax"].cpu().numpy()
+    w.token = synth.apply_prefix_rule(w, argmax)
+    base["token"].copy_(torch.from_numpy(w.token.astype(np.int32)))
+
+    set_bytes = sum(base[k].numel() * base[k].element_size() for k in ("k_cache", "v_cache", "lm_head", "hidden"))
+    R = args.rotate or max(2, math.ceil(4 * MALL_BYTES / set_bytes))
+    sets = [base]
+    for _ in range(R - 1):
+        s = dict(base)
+        for k in ("k_cache", "v_cache", "lm_head", "hidden"):
+            s[k] = base[k].clone()
+        sets.append(s)
+    log(f"[bench] {R} rotated input sets of {set_bytes / 2**20:.1f} MiB")
+
+    stream = torch.cuda.current_stream(dev)
+    for i in range(args.warmup):
+        plan.step(sets[i % R], out, stream=stream, **kw)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    for row in evs:
+        for e in row:
+            e.record(stream)
+    torch.cuda.synchronize()
+    log(f"[bench] timing {K} steps")
+    t0 = time.perf_counter()
+    for i in range(K):
+        plan.step(sets[i % R], out, stream=stream, stage_events=evs[i], **kw)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / K
+
+    st = {"attn": [], "lm": [], "vocab": [], "step": []}
+    for row in evs:
+        st["attn"].append(row[0].elapsed_time(row[1]))
+        st["lm"].append(row[1].elapsed_time(row[2]))
+        st["vocab"].append(row[2].elapsed_time(row[3]))
+        st["step"].append(row[0].elapsed_time(row[3]))
+    avg = {k: float(np.mean(v)) for k, v in st.items()}
+    nb = stage_bytes(w, M, es)
+    stages = {
+        "attention": {"us": avg["attn"] * 1e3, "GB/s": nb["attn"] / (avg["attn"] * 1e-3) / 1e9,
+                      "TFLOP/s": nb["attn_flops"] / (avg["attn"] * 1e-3) / 1e12, "bytes": nb["attn"]},
+        "lm_head": {"us": avg["lm"] * 1e3, "GB/s": nb["lm"] / (avg["lm"] * 1e-3) / 1e9,
+                    "TFLOP/s": nb["lm_flops"] / (avg["lm"] * 1e-3) / 1e12, "bytes": nb["lm"]},
+        "vocab_pass": {"us": avg["vocab"] * 1e3, "GB/s": nb["vocab"] / (avg["vocab"] * 1e-3) / 1e9,
+                       "bytes": nb["vocab"]},
+        "step_events_us": avg["step"] * 1e3,
+    }
+    dom = max(("attention", "lm_head", "vocab_pass"), key=lambda k: stages[k]["us"])
+    achieved = stages[dom]["GB/s"]
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None}
+    if dom == "lm_head":
+        peak_tf = BF16_PEAK_TFLOPS if shp.dtype == "bf16" else FP32_PEAK_TFLOPS
+        roofline["mfma_frac"] = round(stages["lm_head"]["TFLOP/s"] / peak_tf, 4)
+    log(f"[bench] {ms_step * 1e3:.1f} us/step; stages " +
+        ", ".join(f"{k} {stages[k]['us']:.1f} us" for k in ("attention", "lm_head", "vocab_pass")))
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib << 20
+        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        log("[bench] timing the CPU oracle on the host")
+        n_done, t_cpu = 0, 0.0
+        while t_cpu < args.cpu_seconds or n_done == 0:
+            t1 = time.perf_counter()
+            oracle.verify_step(w)
+            t_cpu += time.perf_counter() - t1
+            n_done += 1
+        cpu = {"value": round(n_done / t_cpu, 4), "unit": "steps/s", "cores": oracle.threads(), "kind": "oracle",
+               "sample": f"{n_done} full steps of the same workload (attention, LM head, vocab statistics, "
+                         f"acceptance, path), float64, {t_cpu:.1f} s"}
+
+    wl = {"workload": f"{shp.name}: {shp.dtype}, hidden {shp.hidden}, heads {shp.n_q_heads}/{shp.n_kv_heads}, "
+                      f"head_dim {shp.head_dim}, vocab {shp.vocab}, batch {B}, nodes {M}, "
+                      f"KV len {int(w.kv_len.max())}", "config_index": cfg, "rotated_input_sets": R}
+    res = {
+        "metric": "tree-verify steps/sec (attn+LM-head+accept), % of HBM and MFMA roofline",
+        "value": round(K / wall, 2), "unit": "steps/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if shp.dtype == "bf16" else "f32", "data": "synthetic", "config": wl,
+        "roofline": roofline, "cpu_baseline": cpu,
+        "stages": {k: ({kk: round(vv, 3) for kk, vv in v.items()} if isinstance(v, dict) else round(v, 3))
+                   for k, v in stages.items()},
+        "device": torch.cuda.get_device_name(dev),
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

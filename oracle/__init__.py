@@ -62,6 +62,7 @@ def _lib():
             "respec_oracle_node_flags": (None, [_I32, _P, _P, _P, _P, _I32, _P, _P, _I32,
                                                 ctypes.c_float, _P, _P, _P]),
             "respec_oracle_lookahead": (_I32, [_I32, _P, _P, _I32, _I32]),
+            "respec_oracle_threads": (_I32, []),
             "respec_oracle_path": (None, [_I32, _P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P,
                                           _P, _P, _P]),
         }
@@ -89,6 +90,11 @@ def _dt(w) -> int:
 # ---------------------------------------------------------------------------
 # Stages
 # ---------------------------------------------------------------------------
+
+def threads() -> int:
+    """OpenMP threads used by the oracle's parallel loops."""
+    return int(_lib().respec_oracle_threads())
+
 
 def tree(parent, max_depth: int):
     """(status, depth, anc[n][n], is_leaf) of one sequence's parent array."""
@@ -201,7 +207,8 @@ def path(parent, is_leaf, depth, flags, argmax, max_depth: int, m: int, phi: int
 # Whole step
 # ---------------------------------------------------------------------------
 
-TREE_ERROR = 5   # value of seq_status for a malformed tree (matches the C ABI's code)
+# seq_status values for unusable sequences (the C ABI's status codes)
+TREE_ERROR, CAPACITY_ERROR, TOKEN_ERROR = 5, 6, 9
 
 
 def forward(w, rows_per_seq=None) -> dict:
@@ -252,8 +259,14 @@ def decide(w, z, params=None) -> dict:
         lo, hi = int(w.node_off[b]), int(w.node_off[b + 1])
         s, depth, anc, leaf = tree(w.parent[lo:hi], shp.max_depth)
         tok = w.token[lo:hi]
-        if s != 0 or np.any(tok < 0) or np.any(tok >= shp.vocab):
+        if s != 0:
             status[b] = TREE_ERROR
+            continue
+        if np.any(tok[1:] < 0) or np.any(tok[1:] >= shp.vocab) or np.any(w.src[lo + 1:hi] > 1):
+            status[b] = TOKEN_ERROR
+            continue
+        if int(w.kv_len[b]) < 0 or int(w.kv_len[b]) + (hi - lo) > w.k_cache.shape[2]:
+            status[b] = CAPACITY_ERROR
             continue
         f, lp, rk = node_flags(w.parent[lo:hi], tok, w.src[lo:hi], z32[lo:hi],
                                st["argmax"][lo:hi], st["lse"][lo:hi], p.topk, p.tau)

@@ -34,6 +34,7 @@
  * that step is unpinned beyond the hand-worked cases derived from the prose.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -48,6 +49,9 @@
 #define FLAG_TAU 4u      /* log p(top1) - log p(token) <= tau                   */
 #define FLAG_RELAXED 8u  /* retrieved and TOPK and TAU (Eq. 6-7)                */
 #define FLAG_ON_PATH 16u /* node is on the accepted path (root included)        */
+
+/* Number of OpenMP threads the oracle's parallel loops use. */
+int32_t respec_oracle_threads(void) { return (int32_t)omp_get_max_threads(); }
 
 static double bf16_to_double(uint16_t b) {
     uint32_t u = (uint32_t)b << 16;

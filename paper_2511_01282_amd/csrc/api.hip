@@ -1,0 +1,319 @@
+// Host side of the respec_verify C ABI: plan creation (tiling choices and
+// workspace layout), argument validation and the launch sequence of one
+// verification step.  See include/respec_verify.h for the contract.
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <atomic>
+#include <new>
+
+#include "../../include/respec_verify.h"
+#include "kernels.hpp"
+
+using namespace respec;
+
+struct respec_verify_plan {
+  respec_verify_shape s;
+  int es;                 // bytes per element of the workload dtype
+  int group;              // Hq / Hkv
+  // attention tiling
+  int nb, wr, wk, rows_per_wg, n_rowblk, attn_threads, nsplit_cap;
+  size_t attn_lds;
+  // vocabulary pass
+  int ko, nvchunk_cap;
+  // workspace layout (bytes)
+  size_t off_po, off_pm, off_pl, off_x, off_vm, off_vs, off_vt, off_vam, off_vtv, off_vti, off_cnt;
+  size_t n_cnt_attn, n_cnt_row, n_cnt_seq, total;
+  // the attention kernel's LDS limit is raised on the first step (plan creation stays GPU-free)
+  mutable std::atomic<bool> lds_ready{false};
+};
+
+namespace {
+
+constexpr int kTargetWorkgroups = 512;  // about two per compute unit on a 256-CU MI355X
+constexpr int kMinVocabChunk = 2048;
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
+int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
+bool aligned(const void* p, size_t n) { return ((uintptr_t)p % n) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char* respec_status_string(respec_status st) {
+  switch (st) {
+    case RESPEC_OK: return "ok";
+    case RESPEC_ERR_NULL: return "a required pointer is NULL";
+    case RESPEC_ERR_SHAPE: return "sizes out of the supported range or inconsistent";
+    case RESPEC_ERR_DTYPE: return "unknown dtype";
+    case RESPEC_ERR_PARAM: return "acceptance parameters out of range";
+    case RESPEC_ERR_TREE: return "malformed draft tree";
+    case RESPEC_ERR_CAPACITY: return "batch, nodes or KV length above the plan's capacity";
+    case RESPEC_ERR_HIP: return "HIP call or kernel launch failed";
+    case RESPEC_ERR_WORKSPACE: return "workspace missing or not 256-byte aligned";
+    case RESPEC_ERR_TOKEN: return "draft token or source tag out of range";
+  }
+  return "unknown status";
+}
+
+respec_status respec_verify_check_tree(const int32_t* parent, int32_t n, int32_t max_depth) {
+  if (!parent) return RESPEC_ERR_NULL;
+  if (n < 1 || n > RESPEC_MAX_NODES || max_depth < 0) return RESPEC_ERR_SHAPE;
+  if (parent[0] != -1) return RESPEC_ERR_TREE;
+  int depth[RESPEC_MAX_NODES];
+  depth[0] = 0;
+  for (int j = 1; j < n; ++j) {
+    if (parent[j] < 0 || parent[j] >= j) return RESPEC_ERR_TREE;
+    depth[j] = depth[parent[j]] + 1;
+    if (depth[j] > max_depth) return RESPEC_ERR_TREE;
+  }
+  return RESPEC_OK;
+}
+
+respec_status respec_verify_create(const respec_verify_shape* shape, respec_verify_plan** out) {
+  if (!shape || !out) return RESPEC_ERR_NULL;
+  *out = nullptr;
+  const respec_verify_shape& s = *shape;
+  if (s.dtype != RESPEC_F32 && s.dtype != RESPEC_BF16) return RESPEC_ERR_DTYPE;
+  if (s.head_dim != 64 && s.head_dim != 128) return RESPEC_ERR_SHAPE;
+  if (s.n_q_heads < 1 || s.n_kv_heads < 1 || s.n_q_heads % s.n_kv_heads != 0) return RESPEC_ERR_SHAPE;
+  if ((long long)s.n_q_heads * s.head_dim != s.hidden) return RESPEC_ERR_SHAPE;
+  const int es = s.dtype == RESPEC_BF16 ? 2 : 4;
+  if (((long long)s.hidden * es) % 512 != 0) return RESPEC_ERR_SHAPE;
+  if (s.topk_out < 1 || s.topk_out > RESPEC_MAX_TOPK_OUT || s.vocab < s.topk_out) return RESPEC_ERR_SHAPE;
+  if (s.max_batch < 1 || s.max_nodes < 1 || s.max_nodes > RESPEC_MAX_NODES) return RESPEC_ERR_SHAPE;
+  if (s.max_depth < 0 || s.max_depth > RESPEC_MAX_DEPTH || s.max_kv_len < 0) return RESPEC_ERR_SHAPE;
+  if ((long long)s.max_batch * s.max_nodes > (1ll << 24)) return RESPEC_ERR_SHAPE;
+
+  respec_verify_plan* p = new (std::nothrow) respec_verify_plan();
+  if (!p) return RESPEC_ERR_SHAPE;
+  p->s = s;
+  p->es = es;
+  p->group = s.n_q_heads / s.n_kv_heads;
+
+  // attention: rows of a KV head are (node, head-in-group) pairs
+  const int rmax = s.max_nodes * p->group;
+  int nb, rg;
+  if (rmax <= 64) {
+    nb = cdiv(rmax, 16);
+    rg = 1;
+  } else {
+    const int w3 = cdiv(rmax, 48) * 48 - rmax, w4 = cdiv(rmax, 64) * 64 - rmax;
+    nb = w3 < w4 ? 3 : 4;
+    rg = cdiv(rmax, 16 * nb);
+  }
+  p->nb = nb;
+  p->wr = rg < 4 ? rg : 4;
+  p->n_rowblk = cdiv(rg, p->wr);
+  const int rb = 16 * nb;
+  int wk = 4 / p->wr;
+  if (wk > 128 / (p->wr * rb)) wk = 128 / (p->wr * rb);
+  p->wk = wk < 1 ? 1 : wk;
+  p->rows_per_wg = p->wr * rb;
+  const int nwaves = p->wr * p->wk;
+  p->attn_threads = 64 * nwaves;
+  const size_t vt_bytes = (size_t)nwaves * s.head_dim * (kKvTile + kVtPad) * es;
+  const size_t merge_bytes = p->wk > 1 ? (size_t)nwaves * rb * (s.head_dim + 2) * 4 : 0;
+  p->attn_lds = (size_t)kMaxNodes * 16 + 64 + (vt_bytes > merge_bytes ? vt_bytes : merge_bytes);
+  const long long t_cap = (long long)s.max_kv_len + s.max_nodes;
+  const int per_split = s.n_kv_heads * p->n_rowblk;
+  p->nsplit_cap = clampi(cdiv(kTargetWorkgroups, per_split), 1, cdiv(t_cap, 64 * p->wk));
+
+  p->ko = s.topk_out <= 8 ? 8 : 16;
+  p->nvchunk_cap = clampi(cdiv(s.vocab, kMinVocabChunk), 1, 64);
+
+  // workspace
+  const size_t mcap = (size_t)s.max_batch * s.max_nodes;
+  const size_t prow = (size_t)s.max_batch * s.n_kv_heads * p->n_rowblk * p->nsplit_cap * p->rows_per_wg;
+  const size_t vp = mcap * p->nvchunk_cap;
+  size_t off = 0;
+  p->off_po = off; off = align256(off + prow * s.head_dim * 4);
+  p->off_pm = off; off = align256(off + prow * 4);
+  p->off_pl = off; off = align256(off + prow * 4);
+  p->off_x = off; off = align256(off + mcap * s.hidden * es);
+  p->off_vm = off; off = align256(off + vp * 4);
+  p->off_vs = off; off = align256(off + vp * 4);
+  p->off_vt = off; off = align256(off + vp * 4);
+  p->off_vam = off; off = align256(off + vp * 4);
+  p->off_vtv = off; off = align256(off + vp * p->ko * 4);
+  p->off_vti = off; off = align256(off + vp * p->ko * 4);
+  p->n_cnt_attn = (size_t)s.max_batch * s.n_kv_heads * p->n_rowblk;
+  p->n_cnt_row = mcap;
+  p->n_cnt_seq = s.max_batch;
+  p->off_cnt = off; off = align256(off + (p->n_cnt_attn + p->n_cnt_row + p->n_cnt_seq) * 4);
+  p->total = off;
+
+  *out = p;
+  return RESPEC_OK;
+}
+
+void respec_verify_destroy(respec_verify_plan* plan) { delete plan; }
+
+size_t respec_verify_workspace_bytes(const respec_verify_plan* plan) { return plan ? plan->total : 0; }
+
+respec_status respec_verify_workspace_init(const respec_verify_plan* plan, void* workspace, void* stream) {
+  if (!plan) return RESPEC_ERR_NULL;
+  if (!workspace || !aligned(workspace, 256)) return RESPEC_ERR_WORKSPACE;
+  int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + plan->off_cnt);
+  const size_t n = plan->n_cnt_attn + plan->n_cnt_row + plan->n_cnt_seq;
+  return launch_zero_i32(cnt, n, static_cast<hipStream_t>(stream)) == hipSuccess ? RESPEC_OK : RESPEC_ERR_HIP;
+}
+
+respec_status respec_verify_step(const respec_verify_plan* plan, const respec_verify_args* args, void* workspace,
+                                 void* stream) {
+  if (!plan || !args) return RESPEC_ERR_NULL;
+  const respec_verify_shape& s = plan->s;
+  const respec_verify_args& a = *args;
+  if (!workspace || !aligned(workspace, 256)) return RESPEC_ERR_WORKSPACE;
+  if (a.stop_after < RESPEC_STOP_ALL || a.stop_after > RESPEC_STOP_LOGITS) return RESPEC_ERR_PARAM;
+  if (a.batch < 0) return RESPEC_ERR_SHAPE;
+  if (a.batch > s.max_batch) return RESPEC_ERR_CAPACITY;
+  const bool full = a.stop_after == RESPEC_STOP_ALL;
+  const bool need_logits = a.stop_after != RESPEC_STOP_ATTN;
+  if (full) {
+    const respec_accept_params& q = a.accept;
+    if (q.topk < 1 || q.topk > s.topk_out || !(q.tau >= 0.f) || isinf(q.tau) || q.min_lookahead < 0 ||
+        q.max_relaxed < 0)
+      return RESPEC_ERR_PARAM;
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipEvent_t* ev = static_cast<hipEvent_t*>(a.stage_events);
+  if (a.batch == 0) {
+    if (ev)
+      for (int k = 0; k < 4; ++k)
+        if (hipEventRecord(ev[k], st) != hipSuccess) return RESPEC_ERR_HIP;
+    return RESPEC_OK;
+  }
+  if (a.max_nodes_in_batch < 1 || a.max_kv_len_in_batch < 0) return RESPEC_ERR_SHAPE;
+  if (a.max_nodes_in_batch > s.max_nodes || a.max_kv_len_in_batch > s.max_kv_len) return RESPEC_ERR_CAPACITY;
+  if (a.total_nodes < a.batch || (long long)a.total_nodes > (long long)a.batch * a.max_nodes_in_batch)
+    return RESPEC_ERR_SHAPE;
+  if ((long long)a.kv_capacity < (long long)a.max_kv_len_in_batch + a.max_nodes_in_batch) return RESPEC_ERR_SHAPE;
+  if (!a.node_off || !a.kv_len || !a.hidden || !a.k_cache || !a.v_cache || !a.parent) return RESPEC_ERR_NULL;
+  if (need_logits && (!a.lm_head || !a.logits)) return RESPEC_ERR_NULL;
+  if (full && (!a.token || !a.src || !a.max_logit || !a.lse || !a.entropy || !a.argmax || !a.topk_id ||
+               !a.topk_logprob || !a.tok_logprob || !a.flags || !a.leaf_acc_len || !a.path || !a.acc_len ||
+               !a.bonus || !a.winner_leaf || !a.seq_status))
+    return RESPEC_ERR_NULL;
+  if (!aligned(a.hidden, 16) || !aligned(a.k_cache, 16) || !aligned(a.v_cache, 16) ||
+      (need_logits && (!aligned(a.lm_head, 16) || !aligned(a.logits, 16))) || (a.attn_out && !aligned(a.attn_out, 4)))
+    return RESPEC_ERR_SHAPE;
+
+  char* ws = static_cast<char*>(workspace);
+  int32_t* cnt = reinterpret_cast<int32_t*>(ws + plan->off_cnt);
+
+  if (!plan->lds_ready.load(std::memory_order_acquire)) {
+    if (set_tree_attn_lds_limit(s.dtype, s.head_dim, plan->nb, plan->attn_lds) != hipSuccess) return RESPEC_ERR_HIP;
+    plan->lds_ready.store(true, std::memory_order_release);
+  }
+  if (ev && hipEventRecord(ev[0], st) != hipSuccess) return RESPEC_ERR_HIP;
+
+  // ---- tree-masked attention + residual ----
+  AttnArgs at;
+  at.hidden = a.hidden;
+  at.k_cache = a.k_cache;
+  at.v_cache = a.v_cache;
+  at.node_off = a.node_off;
+  at.kv_len = a.kv_len;
+  at.parent = a.parent;
+  at.part_o = reinterpret_cast<float*>(ws + plan->off_po);
+  at.part_m = reinterpret_cast<float*>(ws + plan->off_pm);
+  at.part_l = reinterpret_cast<float*>(ws + plan->off_pl);
+  at.counter = cnt;
+  at.x_out = ws + plan->off_x;
+  at.attn_out = a.attn_out;
+  at.total_nodes = a.total_nodes;
+  at.hidden_size = s.hidden;
+  at.n_kv_heads = s.n_kv_heads;
+  at.group = plan->group;
+  at.kv_cap = a.kv_capacity;
+  at.max_nodes = a.max_nodes_in_batch;
+  const long long t_max = (long long)a.max_kv_len_in_batch + a.max_nodes_in_batch;
+  const int per_split = a.batch * s.n_kv_heads * plan->n_rowblk;
+  const int target = clampi(cdiv(kTargetWorkgroups, per_split), 1, plan->nsplit_cap);
+  const int step_rows = 64 * plan->wk;
+  at.chunk = cdiv(cdiv(t_max, target), step_rows) * step_rows;
+  at.nsplit = cdiv(t_max, at.chunk);
+  at.n_rowblk = plan->n_rowblk;
+  at.rows_per_wg = plan->rows_per_wg;
+  at.wr = plan->wr;
+  at.wk = plan->wk;
+  at.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.head_dim));
+  dim3 agrid(at.nsplit, s.n_kv_heads * plan->n_rowblk, a.batch);
+  if (launch_tree_attn(s.dtype, s.head_dim, plan->nb, agrid, plan->attn_threads, plan->attn_lds, at, st) !=
+      hipSuccess)
+    return RESPEC_ERR_HIP;
+  if (ev && hipEventRecord(ev[1], st) != hipSuccess) return RESPEC_ERR_HIP;
+
+  // ---- LM head ----
+  if (need_logits) {
+    LmArgs lm;
+    lm.x = ws + plan->off_x;
+    lm.w = a.lm_head;
+    lm.logits = a.logits;
+    lm.m_rows = a.total_nodes;
+    lm.vocab = s.vocab;
+    lm.hidden_size = s.hidden;
+    const int mb = a.total_nodes <= 16 ? 1 : a.total_nodes <= 32 ? 2 : a.total_nodes <= 48 ? 3 : 4;
+    dim3 lgrid(cdiv(s.vocab, 128), cdiv(a.total_nodes, 16 * mb));
+    if (launch_lmhead(s.dtype, mb, lgrid, lm, st) != hipSuccess) return RESPEC_ERR_HIP;
+  }
+  if (ev && hipEventRecord(ev[2], st) != hipSuccess) return RESPEC_ERR_HIP;
+
+  // ---- vocabulary pass, predicates, path ----
+  if (full) {
+    VocabArgs v;
+    v.logits = a.logits;
+    v.node_off = a.node_off;
+    v.kv_len = a.kv_len;
+    v.parent = a.parent;
+    v.token = a.token;
+    v.src = a.src;
+    v.p_m = reinterpret_cast<float*>(ws + plan->off_vm);
+    v.p_s = reinterpret_cast<float*>(ws + plan->off_vs);
+    v.p_t = reinterpret_cast<float*>(ws + plan->off_vt);
+    v.p_am = reinterpret_cast<int32_t*>(ws + plan->off_vam);
+    v.p_tv = reinterpret_cast<float*>(ws + plan->off_vtv);
+    v.p_ti = reinterpret_cast<int32_t*>(ws + plan->off_vti);
+    v.row_counter = cnt + plan->n_cnt_attn;
+    v.seq_counter = cnt + plan->n_cnt_attn + plan->n_cnt_row;
+    v.max_logit = a.max_logit;
+    v.lse = a.lse;
+    v.entropy = a.entropy;
+    v.argmax = a.argmax;
+    v.topk_id = a.topk_id;
+    v.topk_logprob = a.topk_logprob;
+    v.tok_logprob = a.tok_logprob;
+    v.flags = a.flags;
+    v.leaf_acc_len = a.leaf_acc_len;
+    v.path = a.path;
+    v.acc_len = a.acc_len;
+    v.bonus = a.bonus;
+    v.winner_leaf = a.winner_leaf;
+    v.seq_status = a.seq_status;
+    v.total_nodes = a.total_nodes;
+    v.batch = a.batch;
+    v.vocab = s.vocab;
+    int nch = clampi(cdiv(kTargetWorkgroups, a.total_nodes), 1, plan->nvchunk_cap);
+    v.chunk = cdiv(s.vocab, nch);
+    v.nchunk = cdiv(s.vocab, v.chunk);
+    v.topk_out = s.topk_out;
+    v.max_nodes = a.max_nodes_in_batch;
+    v.max_depth = s.max_depth;
+    v.kv_cap = a.kv_capacity;
+    v.max_kv = a.max_kv_len_in_batch;
+    v.topk = a.accept.topk;
+    v.min_lookahead = a.accept.min_lookahead;
+    v.max_relaxed = a.accept.max_relaxed;
+    v.tau = a.accept.tau;
+    dim3 vgrid(v.nchunk, a.total_nodes + a.batch);
+    if (launch_vocab(plan->ko, vgrid, v, st) != hipSuccess) return RESPEC_ERR_HIP;
+  }
+  if (ev && hipEventRecord(ev[3], st) != hipSuccess) return RESPEC_ERR_HIP;
+  return RESPEC_OK;
+}
+
+}  // extern "C"

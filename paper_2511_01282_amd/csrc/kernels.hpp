@@ -1,0 +1,70 @@
+// Internal launch interface of the verification kernels (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace respec {
+
+constexpr int kMaxNodes = 128;   // tree nodes per sequence (ancestor bitsets of 4 words)
+constexpr int kMaxDepth = 64;    // chain bits fit one 64-bit mask
+constexpr int kVtPad = 4;        // elements of padding per transposed-V row in LDS
+constexpr int kKvTile = 32;      // KV rows per wave step in the attention loop
+
+struct AttnArgs {
+  const void* hidden;      // [M][Hd]
+  const void* k_cache;     // [B][Hkv][kv_cap][D]
+  const void* v_cache;
+  const int32_t* node_off; // [B+1]
+  const int32_t* kv_len;   // [B]
+  const int32_t* parent;   // [M]
+  float* part_o;           // [B*Hkv*n_rowblk][nsplit][rows_per_wg][D]
+  float* part_m;           // [B*Hkv*n_rowblk][nsplit][rows_per_wg]   (log2 units)
+  float* part_l;
+  int32_t* counter;        // [B*Hkv*n_rowblk]
+  void* x_out;             // [M][Hd] residual h + O in the workload dtype
+  float* attn_out;         // [M][Hd] or null
+  int32_t total_nodes, hidden_size, n_kv_heads, group, kv_cap, max_nodes;
+  int32_t nsplit, chunk, n_rowblk, rows_per_wg, wr, wk;
+  float scale_log2;        // log2(e) / sqrt(D)
+};
+
+struct LmArgs {
+  const void* x;           // [M][Hd]
+  const void* w;           // [V][Hd]
+  float* logits;           // [M][V]
+  int32_t m_rows, vocab, hidden_size;
+};
+
+struct VocabArgs {
+  const float* logits;     // [M][V]
+  const int32_t* node_off; // [B+1]
+  const int32_t* kv_len;   // [B]
+  const int32_t* parent;
+  const int32_t* token;
+  const uint8_t* src;
+  // per-chunk partials
+  float* p_m; float* p_s; float* p_t; int32_t* p_am;   // [M][nchunk]
+  float* p_tv; int32_t* p_ti;                          // [M][nchunk][KO]
+  int32_t* row_counter;    // [M]
+  int32_t* seq_counter;    // [B]
+  // outputs
+  float* max_logit; float* lse; float* entropy; int32_t* argmax;
+  int32_t* topk_id; float* topk_logprob; float* tok_logprob; uint8_t* flags;
+  int32_t* leaf_acc_len; int32_t* path; int32_t* acc_len; int32_t* bonus; int32_t* winner_leaf;
+  int32_t* seq_status;
+  int32_t total_nodes, batch, vocab, nchunk, chunk, topk_out, max_nodes, max_depth, kv_cap, max_kv;
+  int32_t topk, min_lookahead, max_relaxed;
+  float tau;
+};
+
+// dtype-dispatching launchers (0 = f32, 1 = bf16); return hipSuccess or the launch error
+hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int threads, size_t lds,
+                            const AttnArgs& a, hipStream_t s);
+hipError_t set_tree_attn_lds_limit(int dtype, int head_dim, int nb, size_t lds);
+hipError_t launch_lmhead(int dtype, int mb, dim3 grid, const LmArgs& a, hipStream_t s);
+hipError_t launch_vocab(int ko, dim3 grid, const VocabArgs& a, hipStream_t s);
+hipError_t launch_zero_i32(int32_t* p, size_t n, hipStream_t s);
+
+}  // namespace respec

@@ -1,0 +1,155 @@
+"""The C ABI on the host: exports, plan creation, and argument validation.
+
+None of these calls reaches the GPU: every step call here is rejected by the
+host checks before a kernel is enqueued (fake device addresses are never
+dereferenced on the host).
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "respec_verify.h")
+
+
+@pytest.fixture(scope="module")
+def b():
+    from paper_2511_01282_amd import binding
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2511_01282_amd import build
+        build.build()
+    binding.lib()
+    return binding
+
+
+def _header_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(respec_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function(b):
+    declared = _header_functions()
+    assert set(declared) == set(b.EXPORTS)
+    for name in declared:
+        assert hasattr(b.lib(), name), name
+
+
+def test_status_strings(b):
+    for code in range(10):
+        assert b.status_string(code)
+    assert b.status_string(0) == "ok"
+
+
+@pytest.mark.parametrize("parent,depth,code", [
+    ([-1], 0, 0), ([-1, 0, 1, 1, 0], 2, 0), ([0], 3, 5), ([-1, 1], 3, 5), ([-1, 0, 3, 1], 3, 5),
+    ([-1, 0, 1, 2], 2, 5), ([], 3, 2), (list(range(-1, 128)), 200, 2),
+])
+def test_check_tree(b, parent, depth, code):
+    assert b.check_tree(parent, depth) == code
+
+
+def _shape(b, **over):
+    d = dict(hidden=4096, n_q_heads=32, n_kv_heads=32, head_dim=128, vocab=32000, dtype=b.BF16,
+             max_batch=1, max_nodes=26, max_depth=6, max_kv_len=2048, topk_out=8)
+    d.update(over)
+    return b.Shape(*[d[f] for f, _ in b.Shape._fields_])
+
+
+def _create(b, shape):
+    h = ctypes.c_void_p()
+    st = b.lib().respec_verify_create(ctypes.byref(shape), ctypes.byref(h))
+    return st, h
+
+
+@pytest.mark.parametrize("over,code", [
+    ({}, 0), (dict(dtype=7), 3), (dict(head_dim=96, hidden=32 * 96), 2), (dict(n_kv_heads=5), 2),
+    (dict(hidden=4000), 2), (dict(topk_out=0), 2), (dict(topk_out=17), 2), (dict(vocab=4), 2),
+    (dict(max_nodes=129), 2), (dict(max_nodes=0), 2), (dict(max_depth=65), 2), (dict(max_batch=0), 2),
+    (dict(max_kv_len=-1), 2), (dict(dtype=0, hidden=64, n_q_heads=1, n_kv_heads=1, head_dim=64), 2),
+])
+def test_create_validates_shape(b, over, code):
+    st, h = _create(b, _shape(b, **over))
+    assert st == code
+    if st == 0:
+        assert b.lib().respec_verify_workspace_bytes(h) > 0
+        b.lib().respec_verify_destroy(h)
+    else:
+        assert not h.value
+
+
+def test_workspace_grows_with_capacity(b):
+    _, h1 = _create(b, _shape(b))
+    _, h2 = _create(b, _shape(b, max_batch=8, max_nodes=32, max_kv_len=8192))
+    L = b.lib()
+    assert L.respec_verify_workspace_bytes(h2) > L.respec_verify_workspace_bytes(h1)
+    assert L.respec_verify_workspace_bytes(None) == 0
+    L.respec_verify_destroy(h1)
+    L.respec_verify_destroy(h2)
+    L.respec_verify_destroy(None)
+
+
+FAKE = 0x7F0000000000  # 256-byte aligned fake device address; never dereferenced on the host
+
+
+def _args(b, **over):
+    a = b.Args()
+    a.batch, a.total_nodes, a.max_nodes_in_batch, a.max_kv_len_in_batch = 1, 26, 26, 2048
+    a.kv_capacity, a.stop_after = 2074, 0
+    a.accept = b.AcceptParams(8, 3.0, 2, 2)
+    for f in b.INPUT_FIELDS + b.OUTPUT_FIELDS:
+        setattr(a, f, FAKE)
+    for k, v in over.items():
+        if k in ("topk", "tau", "min_lookahead", "max_relaxed"):
+            setattr(a.accept, k, v)
+        else:
+            setattr(a, k, v)
+    return a
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(stop_after=3), 4), (dict(batch=-1), 2), (dict(batch=2), 6),
+    (dict(topk=0), 4), (dict(topk=9), 4), (dict(tau=-1.0), 4), (dict(tau=float("nan")), 4),
+    (dict(tau=float("inf")), 4), (dict(min_lookahead=-1), 4), (dict(max_relaxed=-1), 4),
+    (dict(max_nodes_in_batch=0), 2), (dict(max_nodes_in_batch=27), 6), (dict(max_kv_len_in_batch=4096), 6),
+    (dict(total_nodes=0), 2), (dict(total_nodes=27), 2), (dict(kv_capacity=2073), 2),
+    (dict(hidden=None), 1), (dict(k_cache=None), 1), (dict(parent=None), 1), (dict(lm_head=None), 1),
+    (dict(logits=None), 1), (dict(token=None), 1), (dict(flags=None), 1), (dict(seq_status=None), 1),
+    (dict(hidden=FAKE + 8), 2), (dict(lm_head=FAKE + 4), 2), (dict(logits=FAKE + 4), 2),
+])
+def test_step_rejects_bad_arguments_before_launch(b, over, code):
+    _, h = _create(b, _shape(b))
+    a = _args(b, **over)
+    assert b.lib().respec_verify_step(h, ctypes.byref(a), FAKE, None) == code
+    b.lib().respec_verify_destroy(h)
+
+
+def test_step_rejects_bad_workspace_and_null_plan(b):
+    _, h = _create(b, _shape(b))
+    a = _args(b)
+    L = b.lib()
+    assert L.respec_verify_step(h, ctypes.byref(a), None, None) == 8
+    assert L.respec_verify_step(h, ctypes.byref(a), FAKE + 16, None) == 8
+    assert L.respec_verify_step(None, ctypes.byref(a), FAKE, None) == 1
+    assert L.respec_verify_step(h, None, FAKE, None) == 1
+    assert L.respec_verify_workspace_init(h, FAKE + 8, None) == 8
+    assert L.respec_verify_workspace_init(None, FAKE, None) == 1
+    L.respec_verify_destroy(h)
+
+
+def test_attention_only_step_needs_no_logit_buffers(b):
+    # stop_after = ATTN with no LM head / logits pointers passes the NULL checks;
+    # an out-of-range accept parameter is then ignored, so only a later check fails
+    _, h = _create(b, _shape(b))
+    a = _args(b, stop_after=1, lm_head=None, logits=None, topk=0, kv_capacity=10)
+    assert b.lib().respec_verify_step(h, ctypes.byref(a), FAKE, None) == 2
+    b.lib().respec_verify_destroy(h)
+
+
+def test_empty_batch_is_a_no_op(b):
+    _, h = _create(b, _shape(b))
+    a = _args(b, batch=0, total_nodes=0)
+    assert b.lib().respec_verify_step(h, ctypes.byref(a), FAKE, None) == 0
+    b.lib().respec_verify_destroy(h)

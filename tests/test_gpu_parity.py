@@ -1,0 +1,196 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Same seeded inputs on both sides.  Bar:
+  - integer and index outputs (argmax, flags, leaf/accepted lengths, paths,
+    bonus, winner, status) bit-exact; top-k ids exact except where the
+    oracle's float32 logits of the two ids are within 1e-4 (then both orders
+    are valid and the id sets must still be valid top-k members);
+  - float outputs (attention O, logits, max logit, lse, entropy, log-probs)
+    within rtol 2e-2 / atol 1e-3 (bf16 inputs, fp32 accumulation); float32
+    workloads additionally within 1e-4.
+Every workload keeps acceptance decisions >= 1e-3 away from their thresholds
+(see tests/workload.py), so the float differences cannot flip a decision.
+"""
+import numpy as np
+import pytest
+
+import respec_synth as synth
+import workload
+
+pytestmark = pytest.mark.gpu
+
+RTOL, ATOL = 2e-2, 1e-3
+
+
+@pytest.fixture(scope="module")
+def rt():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2511_01282_amd import binding, runner
+    binding.lib()
+    return runner
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def compare(case, out, label, check_float=True):
+    e = case.expected
+    w = case.w
+    z32 = case.z.astype(np.float32)
+    if check_float:
+        if out.get("attn_out") is not None:
+            err = np.abs(out["attn_out"] - case.attn).max()
+            _say(f"[{label}] max|dO| = {err:.3e}")
+            np.testing.assert_allclose(out["attn_out"], case.attn, rtol=RTOL, atol=ATOL)
+        err = np.abs(out["logits"] - case.z).max()
+        _say(f"[{label}] max|dz| = {err:.3e}")
+        np.testing.assert_allclose(out["logits"], case.z, rtol=RTOL, atol=ATOL)
+        for k in ("max_logit", "lse", "entropy"):
+            np.testing.assert_allclose(out[k], e[k], rtol=RTOL, atol=ATOL, err_msg=k)
+        np.testing.assert_allclose(out["topk_logprob"], e["topk_logprob"], rtol=RTOL, atol=ATOL)
+        valid = e["seq_status"][_seq_of(w)] == 0
+        nonroot = np.array([w.parent[j] >= 0 for j in range(len(w.parent))]) & valid
+        np.testing.assert_allclose(out["tok_logprob"][nonroot], e["tok_logprob"][nonroot], rtol=RTOL, atol=ATOL)
+        if w.shape.dtype == "f32":
+            np.testing.assert_allclose(out["logits"], case.z, rtol=1e-4, atol=1e-4)
+            np.testing.assert_allclose(out["entropy"], e["entropy"], rtol=1e-4, atol=1e-4)
+    np.testing.assert_array_equal(out["argmax"], e["argmax"], err_msg="argmax")
+    gid, oid = out["topk_id"], e["topk_id"]
+    for r, k in zip(*np.nonzero(gid != oid)):
+        assert abs(float(z32[r, gid[r, k]]) - float(z32[r, oid[r, k]])) < 1e-4, (r, k)
+    for name in ("flags", "leaf_acc_len", "path", "acc_len", "bonus", "winner_leaf", "seq_status"):
+        np.testing.assert_array_equal(out[name], e[name], err_msg=name)
+
+
+def _seq_of(w):
+    seq = np.zeros(len(w.parent), np.int64)
+    for b in range(len(w.node_off) - 1):
+        seq[w.node_off[b]:w.node_off[b + 1]] = b
+    return seq
+
+
+# ---------------------------------------------------------------------------
+# the five workload shapes, at full size
+# ---------------------------------------------------------------------------
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+def test_config_parity(rt, cfg):
+    _say(f"[config {cfg}] building case (seed {synth.SEED_BASE + cfg})")
+    case = workload.build(cfg)
+    _say(f"[config {cfg}] running GPU step: acc_len={case.expected['acc_len'].tolist()}")
+    out = rt.run(case.w)
+    compare(case, out, f"config {cfg}")
+
+
+# ---------------------------------------------------------------------------
+# edge cases
+# ---------------------------------------------------------------------------
+
+def _edge_shape(dtype, hq=4, hkv=2, d=128, v=3000, depth=8, topk_out=8):
+    return synth.Shape("edge", dtype, hq * d, hq, hkv, d, v, 1, 128, depth, topk_out)
+
+
+EDGE = {
+    # name: (dtype, hq, hkv, d, parents, kv_len)
+    "root-only+empty-prefix": ("bf16", 4, 2, 128, [[-1], [-1, 0]], [0, 0]),
+    "ragged-batch": ("bf16", 8, 2, 128, [[-1, 0, 1, 1, 3], [-1], [-1] + list(range(0, 12)), [-1, 0, 0, 0]],
+                     [33, 1, 200, 97]),
+    "chain-causal-f32": ("f32", 2, 1, 64, [[-1] + list(range(0, 20))], [45]),
+    "gqa8-star": ("bf16", 8, 1, 128, [[-1] + [0] * 30], [130]),
+    "d64-bf16-mixed": ("bf16", 4, 4, 64, [[-1, 0, 1, 2, 0, 4, 5, 1, 7]], [64]),
+    "max-nodes-128": ("bf16", 2, 2, 128, [[-1] + [max(0, j - 4) for j in range(1, 128)]], [31]),
+    "max-depth-64": ("bf16", 2, 2, 128, [[-1] + list(range(0, 64))], [5]),
+}
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("name", list(EDGE))
+def test_edge_case_parity(rt, name):
+    dtype, hq, hkv, d, parents, kv = EDGE[name]
+    depth = max(8, max(_depth(p) for p in parents))
+    shp = _edge_shape(dtype, hq, hkv, d, depth=depth)
+    w = synth.custom(shp, parents, kv, seed=101, poison_tail=True)
+    w.shape = synth.Shape("edge", dtype, hq * d, hq, hkv, d, shp.vocab, len(parents),
+                          max(len(p) for p in parents), depth, 8)
+    _say(f"[edge {name}] building")
+    case = workload.finish(w)
+    _say(f"[edge {name}] running GPU step")
+    compare(case, rt.run(case.w), f"edge {name}")
+
+
+def _depth(parent):
+    d = [0] * len(parent)
+    for j in range(1, len(parent)):
+        d[j] = d[parent[j]] + 1
+    return max(d)
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("topk,tau,m,phi", [
+    (1, 3.0, 2, 2), (8, 0.0, 2, 2), (8, 0.5, 1, 3), (8, 1.0, 0, 1), (8, 5.0, 3, 3), (4, 3.0, 0, 0),
+    (16, 2.0, 1, 2),
+])
+def test_accept_parameter_sweep(rt, topk, tau, m, phi):
+    params = synth.AcceptParams(topk=topk, tau=tau, min_lookahead=m, max_relaxed=phi)
+    for cfg in (0,):
+        w = synth.generate(cfg, params=params, poison_tail=True)
+        if topk > 8:
+            w.shape = synth.Shape(w.shape.name, w.shape.dtype, w.shape.hidden, w.shape.n_q_heads,
+                                  w.shape.n_kv_heads, w.shape.head_dim, w.shape.vocab, w.shape.batch,
+                                  w.shape.max_nodes, w.shape.max_depth, 16)
+        _say(f"[sweep cfg{cfg} k={topk} tau={tau} m={m} phi={phi}] building")
+        case = workload.finish(w)
+        compare(case, rt.run(case.w), f"sweep k={topk} tau={tau} m={m} phi={phi}")
+
+
+def test_stop_after_stages(rt):
+    from paper_2511_01282_amd import binding
+    case = workload.build(0)
+    _say("[stop_after] attention only")
+    out = rt.run(case.w, stop_after=binding.STOP_ATTN)
+    np.testing.assert_allclose(out["attn_out"], case.attn, rtol=1e-4, atol=1e-4)
+    _say("[stop_after] through logits")
+    out = rt.run(case.w, stop_after=binding.STOP_LOGITS)
+    np.testing.assert_allclose(out["logits"], case.z, rtol=1e-4, atol=1e-4)
+
+
+@pytest.mark.timeout(300)
+def test_repeated_steps_are_bitwise_identical(rt):
+    case = workload.build(1)
+    plan = rt.make_plan(case.w)
+    inputs = rt.upload(case.w)
+    _say("[repeat] three runs on one plan/workspace")
+    outs = [rt.run(case.w, plan=plan, inputs=inputs, repeat=r) for r in (1, 2, 3)]
+    for o in outs[1:]:
+        for k, v in o.items():
+            if v is not None:
+                np.testing.assert_array_equal(v, outs[0][k], err_msg=k)
+    compare(case, outs[-1], "repeat")
+
+
+def test_invalid_device_data_is_reported_per_sequence(rt):
+    shp = _edge_shape("bf16", 4, 2, 128)
+    parents = [[-1, 0, 1], [-1, 0, 0], [-1, 0, 1], [-1, 0, 1], [-1, 0, 1]]
+    w = synth.custom(shp, parents, [10, 10, 10, 10, 10], seed=7)
+    w.shape = synth.Shape("edge", "bf16", 512, 4, 2, 128, shp.vocab, 5, 3, 8, 8)
+    case = workload.finish(w)
+    bad = case.w
+    bad.parent = bad.parent.copy()
+    bad.token = bad.token.copy()
+    bad.src = bad.src.copy()
+    bad.kv_len = bad.kv_len.copy()
+    bad.parent[3 + 2] = 2          # seq 1: node 2 is its own parent
+    bad.token[6 + 1] = shp.vocab   # seq 2: token out of range
+    bad.src[9 + 2] = 3             # seq 3: unknown source tag
+    bad.kv_len[4] = 10 ** 6        # seq 4: prefix longer than the cache
+    _say("[invalid] running GPU step with malformed sequences 1-4")
+    out = rt.run(bad, step_kw=dict(max_kv_len_in_batch=10))
+    assert out["seq_status"].tolist() == [0, 5, 9, 9, 6]
+    assert out["acc_len"].tolist()[1:] == [-1, -1, -1, -1]
+    assert (out["path"][1:] == -1).all()
+    assert out["acc_len"][0] == case.expected["acc_len"][0]
+    assert out["path"][0].tolist() == case.expected["path"][0].tolist()
