@@ -67,6 +67,8 @@ def main():
     ap.add_argument("--rotate", type=int, default=0, help="input copies rotated per step (0: enough to exceed MALL)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-stage-events", action="store_true",
+                    help="time plain launches only (also reported with stage events otherwise)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -121,6 +123,15 @@ def main():
     torch.cuda.synchronize()
 
     K = args.steps
+    t_plain = None
+    if args.no_stage_events:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(K):
+            plan.step(sets[i % R], out, stream=stream, **kw)
+        torch.cuda.synchronize()
+        t_plain = time.perf_counter() - t0
+        log(f"[bench] plain launches: {t_plain * 1e6 / K:.1f} us/step")
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
     for row in evs:
         for e in row:

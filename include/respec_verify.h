@@ -19,7 +19,8 @@
  *
  * Conventions
  *  - Every tensor pointer in respec_verify_args is caller-owned DEVICE memory.
- *    Functions marked "host" take host pointers.
+ *    Functions marked "host" take host pointers.  hidden, k_cache, v_cache,
+ *    lm_head, logits and attn_out must be 16-byte aligned (RESPEC_ERR_SHAPE).
  *  - The library never allocates, frees or synchronises device memory; a step
  *    only enqueues kernels on the caller's stream (a hipStream_t passed as
  *    void*, NULL = the null stream).  It can be captured in a hipGraph.

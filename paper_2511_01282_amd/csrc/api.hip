@@ -20,19 +20,18 @@ struct respec_verify_plan {
   // attention tiling
   int nb, wr, wk, rows_per_wg, n_rowblk, attn_threads, nsplit_cap;
   size_t attn_lds;
-  // vocabulary pass
-  int ko, nvchunk_cap;
+  // vocabulary statistics: tiles of the LM head and top-K list length
+  int ko, n_vtiles;
   // workspace layout (bytes)
-  size_t off_po, off_pm, off_pl, off_x, off_vm, off_vs, off_vt, off_vam, off_vtv, off_vti, off_cnt;
-  size_t n_cnt_attn, n_cnt_row, n_cnt_seq, total;
+  size_t off_po, off_pm, off_pl, off_x, off_part, off_flag, off_cnt;
+  size_t n_cnt_attn, n_cnt_seq, total;
   // the attention kernel's LDS limit is raised on the first step (plan creation stays GPU-free)
   mutable std::atomic<bool> lds_ready{false};
 };
 
 namespace {
 
-constexpr int kTargetWorkgroups = 512;  // about two per compute unit on a 256-CU MI355X
-constexpr int kMinVocabChunk = 2048;
+constexpr int kTargetWaves = 1024;  // attention: one wave per SIMD on a 256-CU MI355X
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
@@ -115,35 +114,31 @@ respec_status respec_verify_create(const respec_verify_shape* shape, respec_veri
   p->rows_per_wg = p->wr * rb;
   const int nwaves = p->wr * p->wk;
   p->attn_threads = 64 * nwaves;
-  const size_t vt_bytes = (size_t)nwaves * s.head_dim * (kKvTile + kVtPad) * es;
-  const size_t merge_bytes = p->wk > 1 ? (size_t)nwaves * rb * (s.head_dim + 2) * 4 : 0;
-  p->attn_lds = (size_t)kMaxNodes * 16 + 64 + (vt_bytes > merge_bytes ? vt_bytes : merge_bytes);
+  // per wave: two row-major V tiles (bf16, DMA path) or one transposed, padded V tile (float32)
+  const size_t vt_bytes = es == 2 ? (size_t)nwaves * 2 * kKvTile * s.head_dim * es
+                                  : (size_t)nwaves * s.head_dim * (kKvTile + kVtPad) * es;
+  const size_t merge_bytes = p->wk > 1 ? ((size_t)nwaves * rb * (s.head_dim + 2) + (size_t)p->wr * rb) * 4 : 0;
+  p->attn_lds = (size_t)kMaxNodes * 20 + 64 + (vt_bytes > merge_bytes ? vt_bytes : merge_bytes);
   const long long t_cap = (long long)s.max_kv_len + s.max_nodes;
   const int per_split = s.n_kv_heads * p->n_rowblk;
-  p->nsplit_cap = clampi(cdiv(kTargetWorkgroups, per_split), 1, cdiv(t_cap, 64 * p->wk));
+  p->nsplit_cap = clampi(kTargetWaves / (nwaves * per_split), 1, cdiv(t_cap, kKvTile));
 
   p->ko = s.topk_out <= 8 ? 8 : 16;
-  p->nvchunk_cap = clampi(cdiv(s.vocab, kMinVocabChunk), 1, 64);
+  p->n_vtiles = cdiv(s.vocab, kLmTileRows);
 
   // workspace
   const size_t mcap = (size_t)s.max_batch * s.max_nodes;
   const size_t prow = (size_t)s.max_batch * s.n_kv_heads * p->n_rowblk * p->nsplit_cap * p->rows_per_wg;
-  const size_t vp = mcap * p->nvchunk_cap;
   size_t off = 0;
   p->off_po = off; off = align256(off + prow * s.head_dim * 4);
   p->off_pm = off; off = align256(off + prow * 4);
   p->off_pl = off; off = align256(off + prow * 4);
   p->off_x = off; off = align256(off + mcap * s.hidden * es);
-  p->off_vm = off; off = align256(off + vp * 4);
-  p->off_vs = off; off = align256(off + vp * 4);
-  p->off_vt = off; off = align256(off + vp * 4);
-  p->off_vam = off; off = align256(off + vp * 4);
-  p->off_vtv = off; off = align256(off + vp * p->ko * 4);
-  p->off_vti = off; off = align256(off + vp * p->ko * 4);
+  p->off_part = off; off = align256(off + mcap * p->n_vtiles * (4 + 2 * p->ko) * 4);
+  p->off_flag = off; off = align256(off + mcap * 4);
   p->n_cnt_attn = (size_t)s.max_batch * s.n_kv_heads * p->n_rowblk;
-  p->n_cnt_row = mcap;
   p->n_cnt_seq = s.max_batch;
-  p->off_cnt = off; off = align256(off + (p->n_cnt_attn + p->n_cnt_row + p->n_cnt_seq) * 4);
+  p->off_cnt = off; off = align256(off + (p->n_cnt_attn + p->n_cnt_seq) * 4);
   p->total = off;
 
   *out = p;
@@ -158,7 +153,7 @@ respec_status respec_verify_workspace_init(const respec_verify_plan* plan, void*
   if (!plan) return RESPEC_ERR_NULL;
   if (!workspace || !aligned(workspace, 256)) return RESPEC_ERR_WORKSPACE;
   int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + plan->off_cnt);
-  const size_t n = plan->n_cnt_attn + plan->n_cnt_row + plan->n_cnt_seq;
+  const size_t n = plan->n_cnt_attn + plan->n_cnt_seq;
   return launch_zero_i32(cnt, n, static_cast<hipStream_t>(stream)) == hipSuccess ? RESPEC_OK : RESPEC_ERR_HIP;
 }
 
@@ -199,7 +194,7 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
                !a.bonus || !a.winner_leaf || !a.seq_status))
     return RESPEC_ERR_NULL;
   if (!aligned(a.hidden, 16) || !aligned(a.k_cache, 16) || !aligned(a.v_cache, 16) ||
-      (need_logits && (!aligned(a.lm_head, 16) || !aligned(a.logits, 16))) || (a.attn_out && !aligned(a.attn_out, 4)))
+      (need_logits && (!aligned(a.lm_head, 16) || !aligned(a.logits, 16))) || (a.attn_out && !aligned(a.attn_out, 16)))
     return RESPEC_ERR_SHAPE;
 
   char* ws = static_cast<char*>(workspace);
@@ -233,15 +228,15 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   at.max_nodes = a.max_nodes_in_batch;
   const long long t_max = (long long)a.max_kv_len_in_batch + a.max_nodes_in_batch;
   const int per_split = a.batch * s.n_kv_heads * plan->n_rowblk;
-  const int target = clampi(cdiv(kTargetWorkgroups, per_split), 1, plan->nsplit_cap);
-  const int step_rows = 64 * plan->wk;
-  at.chunk = cdiv(cdiv(t_max, target), step_rows) * step_rows;
+  const int target = clampi(kTargetWaves / (plan->attn_threads / 64 * per_split), 1, plan->nsplit_cap);
+  at.chunk = cdiv(cdiv(t_max, target), kKvTile) * kKvTile;
   at.nsplit = cdiv(t_max, at.chunk);
   at.n_rowblk = plan->n_rowblk;
   at.rows_per_wg = plan->rows_per_wg;
   at.wr = plan->wr;
   at.wk = plan->wk;
   at.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.head_dim));
+  at.lds_work_bytes = (int)(plan->attn_lds - (size_t)kMaxNodes * 20 - 64);
   dim3 agrid(at.nsplit, s.n_kv_heads * plan->n_rowblk, a.batch);
   if (launch_tree_attn(s.dtype, s.head_dim, plan->nb, agrid, plan->attn_threads, plan->attn_lds, at, st) !=
       hipSuccess)
@@ -258,28 +253,25 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
     lm.vocab = s.vocab;
     lm.hidden_size = s.hidden;
     const int mb = a.total_nodes <= 16 ? 1 : a.total_nodes <= 32 ? 2 : a.total_nodes <= 48 ? 3 : 4;
-    dim3 lgrid(cdiv(s.vocab, 128), cdiv(a.total_nodes, 16 * mb));
-    if (launch_lmhead(s.dtype, mb, lgrid, lm, st) != hipSuccess) return RESPEC_ERR_HIP;
+    lm.n_mtiles = cdiv(a.total_nodes, 16 * mb);
+    lm.partials = full ? reinterpret_cast<float*>(ws + plan->off_part) : nullptr;
+    lm.n_vtiles = plan->n_vtiles;
+    if (launch_lmhead(s.dtype, mb, plan->ko, lm, st) != hipSuccess) return RESPEC_ERR_HIP;
   }
   if (ev && hipEventRecord(ev[2], st) != hipSuccess) return RESPEC_ERR_HIP;
 
-  // ---- vocabulary pass, predicates, path ----
+  // ---- row statistics, predicates, path ----
   if (full) {
     VocabArgs v;
     v.logits = a.logits;
+    v.partials = reinterpret_cast<const float*>(ws + plan->off_part);
     v.node_off = a.node_off;
     v.kv_len = a.kv_len;
     v.parent = a.parent;
     v.token = a.token;
     v.src = a.src;
-    v.p_m = reinterpret_cast<float*>(ws + plan->off_vm);
-    v.p_s = reinterpret_cast<float*>(ws + plan->off_vs);
-    v.p_t = reinterpret_cast<float*>(ws + plan->off_vt);
-    v.p_am = reinterpret_cast<int32_t*>(ws + plan->off_vam);
-    v.p_tv = reinterpret_cast<float*>(ws + plan->off_vtv);
-    v.p_ti = reinterpret_cast<int32_t*>(ws + plan->off_vti);
-    v.row_counter = cnt + plan->n_cnt_attn;
-    v.seq_counter = cnt + plan->n_cnt_attn + plan->n_cnt_row;
+    v.seq_counter = cnt + plan->n_cnt_attn;
+    v.flag_ws = reinterpret_cast<int32_t*>(ws + plan->off_flag);
     v.max_logit = a.max_logit;
     v.lse = a.lse;
     v.entropy = a.entropy;
@@ -297,9 +289,7 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
     v.total_nodes = a.total_nodes;
     v.batch = a.batch;
     v.vocab = s.vocab;
-    int nch = clampi(cdiv(kTargetWorkgroups, a.total_nodes), 1, plan->nvchunk_cap);
-    v.chunk = cdiv(s.vocab, nch);
-    v.nchunk = cdiv(s.vocab, v.chunk);
+    v.n_vtiles = plan->n_vtiles;
     v.topk_out = s.topk_out;
     v.max_nodes = a.max_nodes_in_batch;
     v.max_depth = s.max_depth;
@@ -309,8 +299,7 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
     v.min_lookahead = a.accept.min_lookahead;
     v.max_relaxed = a.accept.max_relaxed;
     v.tau = a.accept.tau;
-    dim3 vgrid(v.nchunk, a.total_nodes + a.batch);
-    if (launch_vocab(plan->ko, vgrid, v, st) != hipSuccess) return RESPEC_ERR_HIP;
+    if (launch_finalize(plan->ko, a.total_nodes + a.batch, v, st) != hipSuccess) return RESPEC_ERR_HIP;
   }
   if (ev && hipEventRecord(ev[3], st) != hipSuccess) return RESPEC_ERR_HIP;
   return RESPEC_OK;

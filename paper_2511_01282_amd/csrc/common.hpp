@@ -81,6 +81,156 @@ __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
 
+// Top-K candidates as 64-bit keys: the high word is the float's bits mapped to
+// an order-preserving unsigned integer, the low word is the inverted token id,
+// so a larger key is a larger value, or an equal value with a smaller id.
+// Key 0 is below every real candidate and marks an empty slot.
+__device__ __forceinline__ uint32_t ord_f32(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_value(uint64_t k) {
+  const uint32_t u = (uint32_t)(k >> 32);
+  return __uint_as_float((u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u);
+}
+__device__ __forceinline__ int key_id(uint64_t k) { return (int)(~(uint32_t)k); }
+__device__ __forceinline__ uint64_t make_key(float v, int id) {
+  return ((uint64_t)ord_f32(v) << 32) | (uint32_t)(~(uint32_t)id);
+}
+
+// Exact top-K of two descending key lists: the element-wise maxima of a[i] and
+// b[K-1-i] are the top K of the union and form a bitonic sequence, which
+// log2(K) compare-exchange stages sort (bitonic merge).  K is 4, 8 or 16.
+template <int K>
+__device__ __forceinline__ void merge_topk(uint64_t (&a)[K], const uint64_t (&b)[K]) {
+#pragma unroll
+  for (int i = 0; i < K; ++i) a[i] = b[K - 1 - i] > a[i] ? b[K - 1 - i] : a[i];
+#pragma unroll
+  for (int st = K / 2; st >= 1; st >>= 1) {
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+      if ((i & st) == 0) {
+        const int j = i + st;
+        const bool sw = a[j] > a[i];
+        const uint64_t x = a[i], y = a[j];
+        a[i] = sw ? y : x;
+        a[j] = sw ? x : y;
+      }
+    }
+  }
+}
+
+// Online softmax statistics of a set of logits: max m, smallest argmax,
+// S = sum e^(z-m), T = sum e^(z-m) (z-m).  merge() combines two disjoint sets
+// without branches; an empty set has m = -inf.
+struct RowStats {
+  float m, S, T;
+  int am;
+  __device__ __forceinline__ void init() {
+    m = -__builtin_huge_valf();
+    S = 0.f;
+    T = 0.f;
+    am = 0x7FFFFFFF;
+  }
+  __device__ __forceinline__ void merge(float m2, float S2, float T2, int am2) {
+    const float M = fmaxf(m, m2);
+    const bool z1 = m == -__builtin_huge_valf(), z2 = m2 == -__builtin_huge_valf();
+    const float d1 = z1 ? 0.f : m - M, d2 = z2 ? 0.f : m2 - M;
+    const float e1 = z1 ? 0.f : __expf(d1), e2 = z2 ? 0.f : __expf(d2);
+    T = e1 * (T + d1 * S) + e2 * (T2 + d2 * S2);
+    S = e1 * S + e2 * S2;
+    am = m > m2 ? am : (m2 > m ? am2 : min(am, am2));
+    m = M;
+  }
+  template <int LEVEL>
+  __device__ __forceinline__ void merge_level();
+};
+
+// Butterfly partner exchange at level 0..5 of a wave: levels 0-3 pair lanes
+// inside a 16-lane row with DPP moves (xor 1, xor 2, mirror within 8, mirror
+// within 16); levels 4 and 5 pair rows (xor 16, xor 32) with a lane shuffle.
+// After levels 0..L every lane holds the combination of its 2^(L+1) lanes.
+template <int LEVEL>
+__device__ __forceinline__ int xchg(int v) {
+  if constexpr (LEVEL == 0) return __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);   // quad_perm 1,0,3,2
+  if constexpr (LEVEL == 1) return __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);   // quad_perm 2,3,0,1
+  if constexpr (LEVEL == 2) return __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false);  // row_half_mirror
+  if constexpr (LEVEL == 3) return __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, false);  // row_mirror
+  if constexpr (LEVEL == 4) return __shfl_xor(v, 16, 64);
+  return __shfl_xor(v, 32, 64);
+}
+template <int LEVEL>
+__device__ __forceinline__ float xchg(float v) {
+  return __int_as_float(xchg<LEVEL>(__float_as_int(v)));
+}
+template <int LEVEL>
+__device__ __forceinline__ uint64_t xchg(uint64_t v) {
+  const uint32_t lo = (uint32_t)xchg<LEVEL>((int)(uint32_t)v), hi = (uint32_t)xchg<LEVEL>((int)(uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+
+template <int LEVEL>
+__device__ __forceinline__ void RowStats::merge_level() {
+  const float m2 = xchg<LEVEL>(m), S2 = xchg<LEVEL>(S), T2 = xchg<LEVEL>(T);
+  const int am2 = xchg<LEVEL>(am);
+  merge(m2, S2, T2, am2);
+}
+
+// Exchange a sorted top-K key list with the butterfly partner and keep the merged top K.
+template <int K, int LEVEL>
+__device__ __forceinline__ void merge_topk_level(uint64_t (&k)[K]) {
+  uint64_t p[K];
+#pragma unroll
+  for (int i = 0; i < K; ++i) p[i] = xchg<LEVEL>(k[i]);
+  merge_topk<K>(k, p);
+}
+
+// Per-tile partial of the vocabulary statistics of one token row:
+// {m, S, T, argmax, top-K keys (2 words each)}, 4 + 2K words.
+template <int K>
+struct TilePartial {
+  static constexpr int kWords = 4 + 2 * K;
+};
+
+// Cross-workgroup hand-off through global memory on a multi-XCD GPU.
+// Each XCD has its own L2, so data that one workgroup hands to another inside
+// a kernel is written and read with device-coherent (agent-scope) accesses,
+// which the hardware performs at the device coherence point (sc1 bit):
+//   producer: st_dev*(...) for the data, then stores_done() before the
+//             workgroup takes its ticket with a device-scope atomic;
+//   consumer: ld_dev*(...) for the data after winning the ticket.
+// No L2 write-back or invalidate is needed (a __threadfence() on every wave
+// would write back and invalidate the whole L2 under every other workgroup).
+// A location is written by at most one workgroup per step.
+__device__ __forceinline__ void st_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev(int32_t* p, int32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev4(float* p, f32x4 v) {  // p 16-byte aligned
+  unsigned long long* q = reinterpret_cast<unsigned long long*>(p);
+  const unsigned long long lo = ((unsigned long long)__float_as_uint(v.y) << 32) | __float_as_uint(v.x);
+  const unsigned long long hi = ((unsigned long long)__float_as_uint(v.w) << 32) | __float_as_uint(v.z);
+  __hip_atomic_store(q, lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(q + 1, hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int32_t ld_dev(const int32_t* p) {
+  return __hip_atomic_load(const_cast<int32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ f32x4 ld_dev4(const float* p) {
+  unsigned long long* q = reinterpret_cast<unsigned long long*>(const_cast<float*>(p));
+  const unsigned long long lo = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const unsigned long long hi = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return f32x4{__uint_as_float((uint32_t)lo), __uint_as_float((uint32_t)(lo >> 32)), __uint_as_float((uint32_t)hi),
+               __uint_as_float((uint32_t)(hi >> 32))};
+}
+// Wait until this wave's memory operations have completed (stores acknowledged).
+__device__ __forceinline__ void stores_done() { __builtin_amdgcn_s_waitcnt(0); }
+
 // Intra-wave ordering point for LDS data written and read by the same wave.
 __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

@@ -28,6 +28,7 @@ struct AttnArgs {
   int32_t total_nodes, hidden_size, n_kv_heads, group, kv_cap, max_nodes;
   int32_t nsplit, chunk, n_rowblk, rows_per_wg, wr, wk;
   float scale_log2;        // log2(e) / sqrt(D)
+  int32_t lds_work_bytes;  // bytes of the kernel's LDS work area (after the ancestor table)
 };
 
 struct LmArgs {
@@ -35,26 +36,27 @@ struct LmArgs {
   const void* w;           // [V][Hd]
   float* logits;           // [M][V]
   int32_t m_rows, vocab, hidden_size;
+  int32_t n_mtiles;        // tiles of 16*MB token rows
+  float* partials;         // [M][n_vtiles][4 + 2K] per-tile row statistics, or null
+  int32_t n_vtiles;        // vocabulary tiles of 64 rows
 };
 
 struct VocabArgs {
   const float* logits;     // [M][V]
+  const float* partials;   // [M][n_vtiles][4 + 2K] written by the LM-head epilogue
   const int32_t* node_off; // [B+1]
   const int32_t* kv_len;   // [B]
   const int32_t* parent;
   const int32_t* token;
   const uint8_t* src;
-  // per-chunk partials
-  float* p_m; float* p_s; float* p_t; int32_t* p_am;   // [M][nchunk]
-  float* p_tv; int32_t* p_ti;                          // [M][nchunk][KO]
-  int32_t* row_counter;    // [M]
   int32_t* seq_counter;    // [B]
+  int32_t* flag_ws;        // [M] predicate bits handed from row workgroups to the path reducer
   // outputs
   float* max_logit; float* lse; float* entropy; int32_t* argmax;
   int32_t* topk_id; float* topk_logprob; float* tok_logprob; uint8_t* flags;
   int32_t* leaf_acc_len; int32_t* path; int32_t* acc_len; int32_t* bonus; int32_t* winner_leaf;
   int32_t* seq_status;
-  int32_t total_nodes, batch, vocab, nchunk, chunk, topk_out, max_nodes, max_depth, kv_cap, max_kv;
+  int32_t total_nodes, batch, vocab, n_vtiles, topk_out, max_nodes, max_depth, kv_cap, max_kv;
   int32_t topk, min_lookahead, max_relaxed;
   float tau;
 };
@@ -63,8 +65,9 @@ struct VocabArgs {
 hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int threads, size_t lds,
                             const AttnArgs& a, hipStream_t s);
 hipError_t set_tree_attn_lds_limit(int dtype, int head_dim, int nb, size_t lds);
-hipError_t launch_lmhead(int dtype, int mb, dim3 grid, const LmArgs& a, hipStream_t s);
-hipError_t launch_vocab(int ko, dim3 grid, const VocabArgs& a, hipStream_t s);
+hipError_t launch_lmhead(int dtype, int mb, int ko, const LmArgs& a, hipStream_t s);
+constexpr int kLmTileRows = 64;  // vocabulary rows per LM-head workgroup (one statistics tile)
+hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s);
 hipError_t launch_zero_i32(int32_t* p, size_t n, hipStream_t s);
 
 }  // namespace respec
