@@ -24,7 +24,7 @@ struct respec_verify_plan {
   int ko, n_vtiles;
   // workspace layout (bytes)
   size_t off_po, off_pm, off_pl, off_x, off_part, off_flag, off_cnt;
-  size_t n_cnt_attn, n_cnt_seq, total;
+  size_t n_cnt_seq, total;
   // the attention kernel's LDS limit is raised on the first step (plan creation stays GPU-free)
   mutable std::atomic<bool> lds_ready{false};
 };
@@ -114,14 +114,14 @@ respec_status respec_verify_create(const respec_verify_shape* shape, respec_veri
   p->rows_per_wg = p->wr * rb;
   const int nwaves = p->wr * p->wk;
   p->attn_threads = 64 * nwaves;
-  // per wave: two row-major V tiles (bf16, DMA path) or one transposed, padded V tile (float32)
-  const size_t vt_bytes = es == 2 ? (size_t)nwaves * 2 * kKvTile * s.head_dim * es
+  // per wave: one row-major, swizzled V tile (bf16) or one transposed, padded V tile (float32)
+  const size_t vt_bytes = es == 2 ? (size_t)nwaves * kKvTile * s.head_dim * es
                                   : (size_t)nwaves * s.head_dim * (kKvTile + kVtPad) * es;
   const size_t merge_bytes = p->wk > 1 ? ((size_t)nwaves * rb * (s.head_dim + 2) + (size_t)p->wr * rb) * 4 : 0;
-  p->attn_lds = (size_t)kMaxNodes * 20 + 64 + (vt_bytes > merge_bytes ? vt_bytes : merge_bytes);
   const long long t_cap = (long long)s.max_kv_len + s.max_nodes;
   const int per_split = s.n_kv_heads * p->n_rowblk;
   p->nsplit_cap = clampi(kTargetWaves / (nwaves * per_split), 1, cdiv(t_cap, kKvTile));
+  p->attn_lds = vt_bytes > merge_bytes ? vt_bytes : merge_bytes;
 
   p->ko = s.topk_out <= 8 ? 8 : 16;
   p->n_vtiles = cdiv(s.vocab, kLmTileRows);
@@ -136,9 +136,8 @@ respec_status respec_verify_create(const respec_verify_shape* shape, respec_veri
   p->off_x = off; off = align256(off + mcap * s.hidden * es);
   p->off_part = off; off = align256(off + mcap * p->n_vtiles * (4 + 2 * p->ko) * 4);
   p->off_flag = off; off = align256(off + mcap * 4);
-  p->n_cnt_attn = (size_t)s.max_batch * s.n_kv_heads * p->n_rowblk;
   p->n_cnt_seq = s.max_batch;
-  p->off_cnt = off; off = align256(off + (p->n_cnt_attn + p->n_cnt_seq) * 4);
+  p->off_cnt = off; off = align256(off + p->n_cnt_seq * 4);
   p->total = off;
 
   *out = p;
@@ -153,7 +152,7 @@ respec_status respec_verify_workspace_init(const respec_verify_plan* plan, void*
   if (!plan) return RESPEC_ERR_NULL;
   if (!workspace || !aligned(workspace, 256)) return RESPEC_ERR_WORKSPACE;
   int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + plan->off_cnt);
-  const size_t n = plan->n_cnt_attn + plan->n_cnt_seq;
+  const size_t n = plan->n_cnt_seq;
   return launch_zero_i32(cnt, n, static_cast<hipStream_t>(stream)) == hipSuccess ? RESPEC_OK : RESPEC_ERR_HIP;
 }
 
@@ -217,7 +216,6 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   at.part_o = reinterpret_cast<float*>(ws + plan->off_po);
   at.part_m = reinterpret_cast<float*>(ws + plan->off_pm);
   at.part_l = reinterpret_cast<float*>(ws + plan->off_pl);
-  at.counter = cnt;
   at.x_out = ws + plan->off_x;
   at.attn_out = a.attn_out;
   at.total_nodes = a.total_nodes;
@@ -236,11 +234,13 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   at.wr = plan->wr;
   at.wk = plan->wk;
   at.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.head_dim));
-  at.lds_work_bytes = (int)(plan->attn_lds - (size_t)kMaxNodes * 20 - 64);
   dim3 agrid(at.nsplit, s.n_kv_heads * plan->n_rowblk, a.batch);
   if (launch_tree_attn(s.dtype, s.head_dim, plan->nb, agrid, plan->attn_threads, plan->attn_lds, at, st) !=
       hipSuccess)
     return RESPEC_ERR_HIP;
+  const int merge_rows = 256 / (s.head_dim / 4);
+  dim3 mgrid(cdiv(plan->rows_per_wg, merge_rows), a.batch * s.n_kv_heads * plan->n_rowblk);
+  if (launch_attn_merge(s.dtype, s.head_dim, mgrid, at, st) != hipSuccess) return RESPEC_ERR_HIP;
   if (ev && hipEventRecord(ev[1], st) != hipSuccess) return RESPEC_ERR_HIP;
 
   // ---- LM head ----
@@ -270,7 +270,7 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
     v.parent = a.parent;
     v.token = a.token;
     v.src = a.src;
-    v.seq_counter = cnt + plan->n_cnt_attn;
+    v.seq_counter = cnt;
     v.flag_ws = reinterpret_cast<int32_t*>(ws + plan->off_flag);
     v.max_logit = a.max_logit;
     v.lse = a.lse;

@@ -17,15 +17,23 @@
 //     the matrix cores; bf16 P is split into hi + lo bf16 parts so that the
 //     probabilities keep ~16 significant bits (bf16 P alone perturbs x enough
 //     to move logits by ~5e-4);
+//   - each wave keeps two KV tiles in flight while it processes a third;
 //   - waves of a row group are merged in LDS; each workgroup writes an
-//     unnormalised partial (O, max, sum) with device-coherent stores; the last
-//     workgroup of a (b, g, row block) to finish (device-scope ticket) merges
-//     all splits, writes O and x, and resets the ticket to zero for the next
-//     step.
+//     unnormalised partial (O, max, sum) per row;
+//   - a second, wide kernel merges the splits of every row and writes O and
+//     x = round(h + O) (one workgroup alone cannot pull the partials of a
+//     head fast enough: a single CU's memory parallelism caps it at tens of
+//     GB/s).
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace respec {
+
+// Bit ai of a 128-bit ancestor set.
+__device__ __forceinline__ bool anc_has(const u32x4& w, int ai) {
+  const uint32_t word = ai < 64 ? (ai < 32 ? w[0] : w[1]) : (ai < 96 ? w[2] : w[3]);
+  return (word >> (ai & 31)) & 1u;
+}
 
 template <typename T, int D>
 struct AttnTile {
@@ -69,7 +77,7 @@ __device__ __forceinline__ void load_tile(AttnTile<T, D>& t, const char* kbase, 
 template <typename T, int D, int NB>
 __device__ __forceinline__ void process_tile(const AttnTile<T, D>& t, int t0, int kv_hi, int L, T* vt,
                                              const u32x4 (&qf)[NB][D * Elem<T>::kBytes / 64], const int (&qnode)[NB],
-                                             const uint32_t* s_anc, float scale_log2, float (&m_run)[NB],
+                                             const u32x4 (&anc)[NB], float scale_log2, float (&m_run)[NB],
                                              float (&l_run)[NB], f32x4 (&o)[D / 16][NB], int lane) {
   using A = AttnTile<T, D>;
   constexpr int ES = A::ES;
@@ -124,7 +132,7 @@ __device__ __forceinline__ void process_tile(const AttnTile<T, D>& t, int t0, in
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
           bool vis = p < kv_hi;
-          if (vis && ai >= 0) vis = qnode[nb] >= 0 && ((s_anc[qnode[nb] * 4 + (ai >> 5)] >> (ai & 31)) & 1u);
+          if (vis && ai >= 0) vis = qnode[nb] >= 0 && anc_has(anc[nb], ai);
           s[kb][nb][i] = vis ? s[kb][nb][i] : kNegInf;
         }
       }
@@ -136,8 +144,8 @@ __device__ __forceinline__ void process_tile(const AttnTile<T, D>& t, int t0, in
     float tm = kNegInf;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) tm = fmaxf(tm, fmaxf(fmaxf(s[kb][nb][0], s[kb][nb][1]), fmaxf(s[kb][nb][2], s[kb][nb][3])));
-    tm = fmaxf(tm, __shfl_xor(tm, 16, 64));
-    tm = fmaxf(tm, __shfl_xor(tm, 32, 64));
+    tm = fmaxf(tm, xchg<4>(tm));
+    tm = fmaxf(tm, xchg<5>(tm));
     const float mn = fmaxf(m_run[nb], tm * scale_log2);
     const bool none = mn == kNegInf;
     const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(m_run[nb] - mn);
@@ -208,8 +216,12 @@ __device__ __forceinline__ void process_tile(const AttnTile<T, D>& t, int t0, in
 }
 
 // ---------------------------------------------------------------------------
-// bf16 path: V tiles go HBM -> LDS by DMA (global_load_lds, 16 bytes per lane,
-// no registers) and are read back transposed with ds_read_b64_tr_b16.
+// bf16 path: K and V tiles are loaded into registers (16 bytes per lane); V is
+// stored into a per-wave LDS tile and read back transposed with
+// ds_read_b64_tr_b16.  (Staging V by LDS DMA instead would leave DMA and
+// register loads in flight together, which the compiler's wait-count
+// insertion treats as completing out of order: it would wait for every
+// outstanding load before each tile.)
 //
 // LDS tile layout: 32 rows x D bf16, row-major; 16-byte chunk c of row r is
 // stored at chunk position c ^ vswz(r) so that the transposing reads of a
@@ -242,36 +254,43 @@ __device__ __forceinline__ void load_k_bf16(KTile<D>& t, const char* kbase, int 
   }
 }
 
-// DMA one 32-row V tile into the wave's LDS tile (rows >= kv_hi clamped).
+// V rows of one 32-row tile, 16 bytes per lane per piece: piece q of lane l
+// is chunk (q*64 + l) % CPR of row (q*64 + l) / CPR (rows >= kv_hi clamped).
 template <int D>
-__device__ __forceinline__ void dma_v_bf16(unsigned char* vtile, const char* vbase, int t0, int kv_hi, int lane) {
-  constexpr int CPR = D * 2 / 16;      // 16-byte chunks per row
-  constexpr int RPI = 64 / CPR;        // rows per DMA instruction
+struct VTile {
+  static constexpr int CPR = D * 2 / 16;           // 16-byte chunks per row
+  static constexpr int kPieces = kKvTile * CPR / 64;
+  u32x4 v[kPieces];
+};
+
+template <int D>
+__device__ __forceinline__ void load_v_bf16(VTile<D>& t, const char* vbase, int t0, int kv_hi, int lane) {
+  constexpr int CPR = VTile<D>::CPR;
 #pragma unroll
-  for (int q = 0; q < kKvTile / RPI; ++q) {
-    const int r = q * RPI + lane / CPR, slot = lane % CPR;
-    const int p = min(t0 + r, kv_hi - 1);
-    const char* src = vbase + (size_t)p * D * 2 + (size_t)(slot ^ vswz<D>(r)) * 16;
-    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                     (__attribute__((address_space(3))) void*)(vtile + q * 1024), 16, 0, 0);
+  for (int q = 0; q < VTile<D>::kPieces; ++q) {
+    const int idx = q * 64 + lane;
+    const int p = min(t0 + idx / CPR, kv_hi - 1);
+    t.v[q] = ld16(vbase + (size_t)p * D * 2 + (size_t)(idx % CPR) * 16);
   }
 }
 
-template <int D, int NB>
-__device__ __forceinline__ void process_tile_bf16(const KTile<D>& t, const unsigned char* vtile, int t0, int kv_hi,
-                                                  int L, const u32x4 (&qf)[NB][D * 2 / 64], const int (&qnode)[NB],
-                                                  const uint32_t* s_anc, float scale_log2, float (&m_run)[NB],
-                                                  float (&l_run)[NB], f32x4 (&o)[D / 16][NB], int lane) {
-  constexpr int KCH = D * 2 / 64;
-  constexpr int DB = D / 16;
-  const int lr = lane & 15, lg = lane >> 4;
-  typedef float f32x2 __attribute__((ext_vector_type(2)));
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+// Store a V tile row-major into the wave's LDS tile, chunk c of row r at
+// chunk position c ^ vswz(r).
+template <int D>
+__device__ __forceinline__ void store_v_bf16(const VTile<D>& t, unsigned char* vtile, int lane) {
+  constexpr int CPR = VTile<D>::CPR;
+#pragma unroll
+  for (int q = 0; q < VTile<D>::kPieces; ++q) {
+    const int idx = q * 64 + lane;
+    const int r = idx / CPR, c = idx % CPR;
+    *reinterpret_cast<u32x4*>(vtile + r * (D * 2) + (c ^ vswz<D>(r)) * 16) = t.v[q];
+  }
+}
 
-  // S^T = K Q^T (unscaled)
-  f32x4 s[2][NB];
+// S^T = K Q^T of one tile, unscaled: lane holds S[query 16*nb + lr][kv t0 + 16*kb + 4*lg + i].
+template <int D, int NB>
+__device__ __forceinline__ void scores_bf16(const KTile<D>& t, const u32x4 (&qf)[NB][D * 2 / 64], f32x4 (&s)[2][NB]) {
+  constexpr int KCH = D * 2 / 64;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
@@ -282,6 +301,40 @@ __device__ __forceinline__ void process_tile_bf16(const KTile<D>& t, const unsig
       s[kb][nb] = acc;
     }
   }
+}
+
+// V^T fragments of one LDS tile: vf[db] is the A operand of O^T += V^T P^T for
+// output rows 16*db .. 16*db+15 (transposing reads, layout described above).
+template <int D>
+__device__ __forceinline__ void read_vt_bf16(const unsigned char* vtile, int lane, u32x4 (&vf)[D / 16]) {
+  constexpr int DB = D / 16;
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int r = 4 * lg + lr / 4;  // row for kb = 0; kb = 1 adds 16 rows (same swizzle)
+  const int sw = vswz<D>(r);
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const int col = 16 * db + 4 * (lr % 4);
+    const unsigned char* addr = vtile + r * (D * 2) + ((col >> 3) ^ sw) * 16 + (col & 7) * 2;
+    const u32x2 h0 = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(addr)));
+    const u32x2 h1 =
+        __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(addr + 16 * D * 2)));
+    vf[db] = u32x4{h0.x, h0.y, h1.x, h1.y};
+  }
+}
+
+// Tree / range mask, online softmax and O^T += V^T P^T for one tile whose
+// scores are in s and whose V^T fragments are in vf.
+template <int D, int NB>
+__device__ __forceinline__ void softmax_pv_bf16(f32x4 (&s)[2][NB], const u32x4 (&vf)[D / 16], int t0, int kv_hi,
+                                                int L, const int (&qnode)[NB], const u32x4 (&anc)[NB],
+                                                float scale_log2, float (&m_run)[NB], float (&l_run)[NB],
+                                                f32x4 (&o)[D / 16][NB], int lane) {
+  constexpr int DB = D / 16;
+  const int lg = lane >> 4;
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   if (t0 + kKvTile > kv_hi || t0 + kKvTile > L) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -292,7 +345,7 @@ __device__ __forceinline__ void process_tile_bf16(const KTile<D>& t, const unsig
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
           bool vis = p < kv_hi;
-          if (vis && ai >= 0) vis = qnode[nb] >= 0 && ((s_anc[qnode[nb] * 4 + (ai >> 5)] >> (ai & 31)) & 1u);
+          if (vis && ai >= 0) vis = qnode[nb] >= 0 && anc_has(anc[nb], ai);
           s[kb][nb][i] = vis ? s[kb][nb][i] : kNegInf;
         }
       }
@@ -304,8 +357,8 @@ __device__ __forceinline__ void process_tile_bf16(const KTile<D>& t, const unsig
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
       tm = fmaxf(tm, fmaxf(fmaxf(s[kb][nb][0], s[kb][nb][1]), fmaxf(s[kb][nb][2], s[kb][nb][3])));
-    tm = fmaxf(tm, __shfl_xor(tm, 16, 64));
-    tm = fmaxf(tm, __shfl_xor(tm, 32, 64));
+    tm = fmaxf(tm, xchg<4>(tm));
+    tm = fmaxf(tm, xchg<5>(tm));
     const float mn = fmaxf(m_run[nb], tm * scale_log2);
     const bool none = mn == kNegInf;
     const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(m_run[nb] - mn);
@@ -339,26 +392,57 @@ __device__ __forceinline__ void process_tile_bf16(const KTile<D>& t, const unsig
       plo[nb][j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{r0, r1}, bf16x2));
     }
   }
-  // V^T fragments by transposing LDS reads
-  const int j = lr;
 #pragma unroll
   for (int db = 0; db < DB; ++db) {
-    u32x2 half[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const int r = 16 * kb + 4 * lg + j / 4;
-      const int col = 16 * db + 4 * (j % 4);
-      const int chunk = (col >> 3) ^ vswz<D>(r);
-      const unsigned char* addr = vtile + r * (D * 2) + chunk * 16 + (col & 7) * 2;
-      const bf16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(addr));
-      half[kb] = __builtin_bit_cast(u32x2, v);
-    }
-    const u32x4 af = {half[0].x, half[0].y, half[1].x, half[1].y};
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      o[db][nb] = mma_k64(bf16_t{}, af, phi[nb], o[db][nb]);
-      o[db][nb] = mma_k64(bf16_t{}, af, plo[nb], o[db][nb]);
+      o[db][nb] = mma_k64(bf16_t{}, vf[db], phi[nb], o[db][nb]);
+      o[db][nb] = mma_k64(bf16_t{}, vf[db], plo[nb], o[db][nb]);
     }
+  }
+}
+
+// Ancestor-or-self bitsets of each lane's query nodes, walked up the parent
+// array held in registers (lane l holds parent[l] and parent[l + 64]); all
+// lanes take part in every exchange and the walk ends when every lane has
+// reached the root or an invalid parent (parents must strictly decrease).
+template <int NB>
+__device__ __forceinline__ void ancestor_bits(const int (&qnode)[NB], int p_lo, int p_hi, int n_nodes,
+                                              u32x4 (&anc)[NB]) {
+  // Take the parents out of the loads' bookkeeping here, in straight-line
+  // code: the compiler then waits for these two loads only, not (as it does
+  // for loaded values used in a load-free loop) for every load in flight.
+  asm volatile("" : "+v"(p_lo), "+v"(p_hi));
+  const int lane = (int)(threadIdx.x & 63);
+  p_lo = lane < n_nodes ? p_lo : -1;
+  p_hi = lane + 64 < n_nodes ? p_hi : -1;
+  int x[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    x[nb] = qnode[nb];
+    anc[nb] = u32x4{0u, 0u, 0u, 0u};
+  }
+  for (int step = 0; step < kMaxNodes; ++step) {
+    bool any = false;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int xv = x[nb];
+      if (xv >= 0) {
+        const uint32_t bit = 1u << (xv & 31);
+        const int w = xv >> 5;
+        anc[nb][0] |= w == 0 ? bit : 0u;
+        anc[nb][1] |= w == 1 ? bit : 0u;
+        anc[nb][2] |= w == 2 ? bit : 0u;
+        anc[nb][3] |= w == 3 ? bit : 0u;
+      }
+      const int sel = (xv & 63) << 2;
+      const int pl = __builtin_amdgcn_ds_bpermute(sel, p_lo);
+      const int ph = __builtin_amdgcn_ds_bpermute(sel, p_hi);
+      const int p = xv >= 64 ? ph : pl;
+      x[nb] = (xv > 0 && p >= 0 && p < xv) ? p : -1;
+      any |= x[nb] >= 0;
+    }
+    if (!__any(any)) break;
   }
 }
 
@@ -367,16 +451,14 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
   constexpr int ES = Elem<T>::kBytes;
   constexpr int KCH = D * ES / 64;     // 64-byte K-chunks per head row
   constexpr int DB = D / 16;           // 16-wide output blocks along D
-  constexpr int VTS = kKvTile + kVtPad;  // elements per transposed-V row
+  constexpr int VTS = kKvTile + kVtPad;  // elements per transposed-V row (float32 path)
   constexpr int RB = 16 * NB;          // query rows per wave
 
   extern __shared__ __align__(16) unsigned char smem[];
-  uint32_t* s_anc = reinterpret_cast<uint32_t*>(smem);                 // [kMaxNodes][4]
-  int* s_par = reinterpret_cast<int*>(smem + kMaxNodes * 16);          // [kMaxNodes]
-  int* s_ticket = reinterpret_cast<int*>(smem + kMaxNodes * 20);       // [1]
-  unsigned char* s_work = smem + kMaxNodes * 20 + 64;
+  unsigned char* s_work = smem;
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar branches below
   const int lr = lane & 15, lg = lane >> 4;
   const int nwaves = blockDim.x >> 6;
   const int wr = wave % a.wr, wk = wave / a.wr;
@@ -401,66 +483,33 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
   const int kv_lo = split * a.chunk;
   const int kv_hi = min(kv_lo + a.chunk, t_rows);
   const int t_first = kv_lo + wk * kKvTile, t_step = kKvTile * a.wk;
+  const int n_tiles = t_first < kv_hi ? (kv_hi - t_first + t_step - 1) / t_step : 0;
 
-  // Query fragments (lane row r = row_wave + 16*nb + lr) and the first tile, issued first.
+  // Issue order (the vector-memory counter drains in order): parents, queries,
+  // then the first two KV tiles.
+  const int p_lo = a.parent[node0 + min(lane, n_nodes - 1)];  // parent[lane] (valid lanes)
+  const int p_hi = a.parent[node0 + min(lane + 64, n_nodes - 1)];
   const int row_wave = row_wg + wr * RB;
   u32x4 qf[NB][KCH];
   int qnode[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
+    // rows past the group's last are loaded from the first row (issued by every lane, so
+    // that every lane's loads are counted alike) and zeroed
     const int r = row_wave + 16 * nb + lr;
-    qnode[nb] = -1;
-    if (r < R) {
-      const int node = r / a.group;
-      const int h = g * a.group + (r - node * a.group);
-      qnode[nb] = node;
-      const char* src = reinterpret_cast<const char*>(a.hidden) +
-                        ((size_t)(node0 + node) * a.hidden_size + (size_t)h * D) * ES;
+    const bool live = r < R;
+    const int rc = live ? r : 0;
+    const int node = rc / a.group;
+    const int h = g * a.group + (rc - node * a.group);
+    qnode[nb] = live ? node : -1;
+    const char* src = reinterpret_cast<const char*>(a.hidden) +
+                      ((size_t)(node0 + node) * a.hidden_size + (size_t)h * D) * ES;
 #pragma unroll
-      for (int kc = 0; kc < KCH; ++kc) qf[nb][kc] = ld16(src + kc * 64 + lg * 16);
-    } else {
-#pragma unroll
-      for (int kc = 0; kc < KCH; ++kc) qf[nb][kc] = u32x4{0, 0, 0, 0};
+    for (int kc = 0; kc < KCH; ++kc) {
+      const u32x4 v = ld16(src + kc * 64 + lg * 16);
+      qf[nb][kc] = live ? v : u32x4{0, 0, 0, 0};
     }
   }
-  [[maybe_unused]] AttnTile<T, D> ta;
-  [[maybe_unused]] AttnTile<T, D> tb;
-  [[maybe_unused]] KTile<D> ka;
-  [[maybe_unused]] KTile<D> kb2;
-  unsigned char* vtiles = s_work + (size_t)wave * 2 * kKvTile * D * ES;  // bf16: two V tiles per wave
-  if constexpr (ES == 2) {
-    if (t_first < kv_hi) {
-      load_k_bf16<D>(ka, kbase, t_first, kv_hi, lane);
-      dma_v_bf16<D>(vtiles, vbase, t_first, kv_hi, lane);
-    }
-  } else {
-    if (t_first < kv_hi) load_tile<T, D>(ta, kbase, vbase, t_first, kv_hi, lane);
-  }
-
-  // Ancestor-or-self bitsets of the sequence's nodes, from the parent array in LDS.
-  for (int t = threadIdx.x; t < n_nodes; t += blockDim.x) s_par[t] = a.parent[node0 + t];
-  __syncthreads();
-  for (int t = threadIdx.x; t < n_nodes; t += blockDim.x) {
-    uint32_t w0 = 0, w1 = 0, w2 = 0, w3 = 0;
-    int x = t;
-    for (int step = 0; step < kMaxNodes; ++step) {
-      const uint32_t bit = 1u << (x & 31);
-      const int word = x >> 5;
-      w0 |= word == 0 ? bit : 0u;
-      w1 |= word == 1 ? bit : 0u;
-      w2 |= word == 2 ? bit : 0u;
-      w3 |= word == 3 ? bit : 0u;
-      if (x == 0) break;
-      const int p = s_par[x];
-      if (p < 0 || p >= x) break;
-      x = p;
-    }
-    s_anc[t * 4 + 0] = w0;
-    s_anc[t * 4 + 1] = w1;
-    s_anc[t * 4 + 2] = w2;
-    s_anc[t * 4 + 3] = w3;
-  }
-  __syncthreads();
 
   float m_run[NB], l_run[NB];
   f32x4 o[DB][NB];
@@ -471,43 +520,67 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int db = 0; db < DB; ++db) o[db][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  u32x4 anc[NB];
 
   if constexpr (ES == 2) {
-    // Two tiles in flight: wait for tile k (K in registers, V in LDS), issue tile k+1, process k.
-    constexpr int VT = kKvTile * D * 2;
-    for (int t0 = t_first; t0 < kv_hi; t0 += 2 * t_step) {
-      const int t1 = t0 + t_step;
-      __builtin_amdgcn_s_waitcnt(0);
+    // Two tiles in flight per wave, all in registers: K fragments go straight
+    // to the matrix cores; V is written to the wave's LDS tile and read back
+    // transposed.  Tile i is waited for, its scores and V^T fragments taken,
+    // and tile i+2 is issued into the registers it frees, so two tiles stream
+    // while tile i is processed.  Past the last tile the issue repeats the
+    // split's last row (cache hits, results unused), which keeps the count of
+    // loads behind every tile constant.
+    unsigned char* vt = s_work + (size_t)wave * kKvTile * D * 2;
+    const int t_last = max(kv_hi - 1, 0);
+    auto tile_row = [&](int i) { return i < n_tiles ? t_first + i * t_step : t_last; };
+    KTile<D> ka, kb;
+    VTile<D> va, vb;
+    // (kv_hi >= 1 always: the sequence has a node, and a split starts before its end or
+    // is clipped to it; so every clamped row below is a valid cache row)
+    // (scheduling barriers keep tile 0's loads ahead of tile 1's: the loop's
+    // wait counts assume that order)
+    load_k_bf16<D>(ka, kbase, tile_row(0), kv_hi, lane);
+    load_v_bf16<D>(va, vbase, tile_row(0), kv_hi, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    load_k_bf16<D>(kb, kbase, tile_row(1), kv_hi, lane);
+    load_v_bf16<D>(vb, vbase, tile_row(1), kv_hi, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    ancestor_bits<NB>(qnode, p_lo, p_hi, n_nodes, anc);  // needs the parents only, while the tiles stream
+    // one tile: scores from K, V through LDS, then the tile two ahead issued into the freed registers
+    auto tile_step = [&](KTile<D>& kt, VTile<D>& vv, int i) {
+      f32x4 s[2][NB];
+      scores_bf16<D, NB>(kt, qf, s);
+      store_v_bf16<D>(vv, vt, lane);
       wave_lds_sync();
-      if (t1 < kv_hi) {
-        load_k_bf16<D>(kb2, kbase, t1, kv_hi, lane);
-        dma_v_bf16<D>(vtiles + VT, vbase, t1, kv_hi, lane);
-      }
-      process_tile_bf16<D, NB>(ka, vtiles, t0, kv_hi, L, qf, qnode, s_anc, a.scale_log2, m_run, l_run, o, lane);
-      if (t1 >= kv_hi) break;
-      const int t2 = t1 + t_step;
-      __builtin_amdgcn_s_waitcnt(0);
-      wave_lds_sync();
-      if (t2 < kv_hi) {
-        load_k_bf16<D>(ka, kbase, t2, kv_hi, lane);
-        dma_v_bf16<D>(vtiles, vbase, t2, kv_hi, lane);
-      }
-      process_tile_bf16<D, NB>(kb2, vtiles + VT, t1, kv_hi, L, qf, qnode, s_anc, a.scale_log2, m_run, l_run, o,
-                               lane);
+      u32x4 vf[DB];
+      read_vt_bf16<D>(vt, lane, vf);
+      load_k_bf16<D>(kt, kbase, tile_row(i + 2), kv_hi, lane);
+      load_v_bf16<D>(vv, vbase, tile_row(i + 2), kv_hi, lane);
+      softmax_pv_bf16<D, NB>(s, vf, t_first + i * t_step, kv_hi, L, qnode, anc, a.scale_log2, m_run, l_run, o, lane);
+      wave_lds_sync();  // this tile's V^T reads precede the next tile's writes
+    };
+    int i = 0;
+    for (; i + 1 < n_tiles; i += 2) {  // no exit between the halves: every path around the loop issues two tiles
+      tile_step(ka, va, i);
+      tile_step(kb, vb, i + 1);
     }
+    if (i < n_tiles) tile_step(ka, va, i);
   } else {
-    T* vt = reinterpret_cast<T*>(s_work + (size_t)wave * D * VTS * ES);
     // float32: registers hold one tile; V is transposed through LDS by the VALU
-    for (int t0 = t_first; t0 < kv_hi; t0 += t_step) {
-      if (t0 != t_first) load_tile<T, D>(ta, kbase, vbase, t0, kv_hi, lane);
-      process_tile<T, D, NB>(ta, t0, kv_hi, L, vt, qf, qnode, s_anc, a.scale_log2, m_run, l_run, o, lane);
+    ancestor_bits<NB>(qnode, p_lo, p_hi, n_nodes, anc);
+    T* vt = reinterpret_cast<T*>(s_work + (size_t)wave * D * VTS * ES);
+    AttnTile<T, D> ta;
+    for (int i = 0; i < n_tiles; ++i) {
+      const int t0 = t_first + i * t_step;
+      load_tile<T, D>(ta, kbase, vbase, t0, kv_hi, lane);
+      process_tile<T, D, NB>(ta, t0, kv_hi, L, vt, qf, qnode, anc, a.scale_log2, m_run, l_run, o, lane);
     }
   }
 
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    l_run[nb] += __shfl_xor(l_run[nb], 16, 64);
-    l_run[nb] += __shfl_xor(l_run[nb], 32, 64);
+    l_run[nb] += xchg<4>(l_run[nb]);
+    l_run[nb] += xchg<5>(l_run[nb]);
   }
 
   // ---- workgroup partial: (O unnormalised, max, sum) per row ----
@@ -518,18 +591,18 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
     for (int nb = 0; nb < NB; ++nb) {
       const int rl = wr * RB + 16 * nb + lr;
 #pragma unroll
-      for (int db = 0; db < DB; ++db) st_dev4(a.part_o + (pbase + rl) * D + 16 * db + 4 * lg, o[db][nb]);
+      for (int db = 0; db < DB; ++db)
+        *reinterpret_cast<f32x4*>(a.part_o + (pbase + rl) * D + 16 * db + 4 * lg) = o[db][nb];
       if (lg == 0) {
-        st_dev(a.part_m + pbase + rl, m_run[nb]);
-        st_dev(a.part_l + pbase + rl, l_run[nb]);
+        a.part_m[pbase + rl] = m_run[nb];
+        a.part_l[pbase + rl] = l_run[nb];
       }
     }
   } else {
-    __syncthreads();  // every wave is done with its V^T tile
+    __syncthreads();  // every wave is done with its V tiles
     float* mo = reinterpret_cast<float*>(s_work);  // [nwaves][RB][D]
     float* mm = mo + (size_t)nwaves * RB * D;     // [nwaves][RB]   then weights
     float* ml = mm + nwaves * RB;                 // [nwaves][RB]
-    float* mL = ml + nwaves * RB;                 // [wr][RB] merged sums
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const int rr = 16 * nb + lr;
@@ -554,9 +627,8 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
         Ls += ml[wv * RB + rr] * wgt;
         mm[wv * RB + rr] = wgt;
       }
-      mL[rl] = Ls;
-      st_dev(a.part_m + pbase + rl, M);
-      st_dev(a.part_l + pbase + rl, Ls);
+      a.part_m[pbase + rl] = M;
+      a.part_l[pbase + rl] = Ls;
     }
     __syncthreads();
     constexpr int D4 = D / 4;
@@ -568,78 +640,78 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
         const int wv = gr + a.wr * k;
         acc += *reinterpret_cast<const f32x4*>(mo + ((size_t)wv * RB + rr) * D + d) * mm[wv * RB + rr];
       }
-      st_dev4(a.part_o + (pbase + rl) * D + d, acc);
+      *reinterpret_cast<f32x4*>(a.part_o + (pbase + rl) * D + d) = acc;
     }
   }
+}
 
-  // ---- completion ticket; the last split merges ----
-  stores_done();
-  __syncthreads();
-  if (threadIdx.x == 0) *s_ticket = atomicAdd(a.counter + bgr, 1);
-  __syncthreads();
-  if (*s_ticket != a.nsplit - 1) return;
-  if (threadIdx.x == 0) st_dev(a.counter + bgr, 0);
+// Split merge and residual: one workgroup per (sequence, KV head, row block,
+// chunk of 256 / (D/4) rows); each thread owns one (row, 4-column) item and
+// requests the partials, maxima and sums of 8 splits at a time.
+//   w_s = 2^(m_s - M) / sum_s' l_s' 2^(m_s' - M),  M = max_s m_s;
+//   O = sum_s w_s O_s;  x = round(h + O).
+// The partials come from the attention kernel that ran before it on the same
+// stream, so plain loads see them.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
+  constexpr int D4 = D / 4;
+  constexpr int kRows = 256 / D4;   // rows per workgroup
+  constexpr int kBatch = 8;         // splits requested per batch
+  const int bgr = blockIdx.y;
+  const int rb = bgr % a.n_rowblk, g = (bgr / a.n_rowblk) % a.n_kv_heads, b = bgr / (a.n_rowblk * a.n_kv_heads);
+  const int node0 = a.node_off[b], node1 = a.node_off[b + 1];
+  int n_nodes = node1 - node0;
+  if (node0 < 0 || node1 > a.total_nodes || n_nodes < 1 || n_nodes > a.max_nodes) n_nodes = 0;
+  const int R = n_nodes * a.group;
+  const int row_wg = rb * a.rows_per_wg;
+  const int rl = blockIdx.x * kRows + (int)threadIdx.x / D4;  // row within the row block
+  const int d = ((int)threadIdx.x % D4) * 4;
+  if (rl >= a.rows_per_wg || row_wg + rl >= R) return;
+  const size_t sbase = (size_t)bgr * a.nsplit * a.rows_per_wg + rl;
+  const size_t sstride = (size_t)a.rows_per_wg;
 
-  // Final merge over splits, in row chunks whose (row, split) weights fit the work area:
-  // w[r][s] = 2^(m_s - M) / sum_s' l_s' 2^(m_s' - M);  O[r][d] = sum_s w[r][s] * O_s[r][d].
-  const int rows_here = min(a.rows_per_wg, R - row_wg);
-  const size_t sbase = (size_t)bgr * a.nsplit * a.rows_per_wg;
-  float* s_w = reinterpret_cast<float*>(s_work);
-  const int work_floats = (int)((a.lds_work_bytes) / 4);
-  const int rc_max = max(1, min(rows_here, work_floats / (2 * a.nsplit)));
-  for (int r0 = 0; r0 < rows_here; r0 += rc_max) {
-    const int rc = min(rc_max, rows_here - r0);
-    __syncthreads();
-    float* s_l = s_w + rc * a.nsplit;
-    for (int idx = threadIdx.x; idx < rc * a.nsplit; idx += blockDim.x) {
-      const int r = idx / a.nsplit, sp = idx - r * a.nsplit;
-      const size_t pr = sbase + (size_t)sp * a.rows_per_wg + r0 + r;
-      s_w[idx] = ld_dev(a.part_m + pr);
-      s_l[idx] = ld_dev(a.part_l + pr);
-    }
-    __syncthreads();
-    for (int r = threadIdx.x; r < rc; r += blockDim.x) {
-      float M = kNegInf;
-      for (int sp = 0; sp < a.nsplit; ++sp) M = fmaxf(M, s_w[r * a.nsplit + sp]);
-      float Ls = 0.f;
-      for (int sp = 0; sp < a.nsplit; ++sp) {
-        const float e = __builtin_amdgcn_exp2f(s_w[r * a.nsplit + sp] - M);
-        s_w[r * a.nsplit + sp] = e;
-        Ls += e * s_l[r * a.nsplit + sp];
-      }
-      const float inv = 1.f / Ls;
-      for (int sp = 0; sp < a.nsplit; ++sp) s_w[r * a.nsplit + sp] *= inv;
-    }
-    __syncthreads();
-    constexpr int D4 = D / 4;
-    constexpr int kBatch = 8;  // split partials loaded per batch, all issued before use
-    for (int idx = threadIdx.x; idx < rc * D4; idx += blockDim.x) {
-      const int r = idx / D4, d = (idx - r * D4) * 4;
-      const float* wgt = s_w + r * a.nsplit;
-      const float* po = a.part_o + (sbase + r0 + r) * D + d;
-      const size_t sstride = (size_t)a.rows_per_wg * D;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      for (int sp0 = 0; sp0 < a.nsplit; sp0 += kBatch) {
-        f32x4 buf[kBatch];
+  const int rr = row_wg + rl;
+  const int node = rr / a.group;
+  const int h = g * a.group + (rr - node * a.group);
+  const size_t gi = (size_t)(node0 + node) * a.hidden_size + (size_t)h * D + d;
+  f32x4 hv;
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u)
-          buf[u] = sp0 + u < a.nsplit ? ld_dev4(po + (size_t)(sp0 + u) * sstride) : f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < 4; ++i) hv[i] = Elem<T>::to_f32(a.hidden, gi + i);
+
+  float M = kNegInf, Ls = 0.f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int sp0 = 0; sp0 < a.nsplit; sp0 += kBatch) {
+    float mv[kBatch], lv[kBatch];
+    f32x4 ov[kBatch];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u)
-          if (sp0 + u < a.nsplit) acc += buf[u] * wgt[sp0 + u];
-      }
-      const int rr = row_wg + r0 + r;
-      const int node = rr / a.group;
-      const int h = g * a.group + (rr - node * a.group);
-      const size_t gi = (size_t)(node0 + node) * a.hidden_size + (size_t)h * D + d;
-      if (a.attn_out) *reinterpret_cast<f32x4*>(a.attn_out + gi) = acc;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float hv = Elem<T>::to_f32(a.hidden, gi + i);
-        Elem<T>::store(a.x_out, gi + i, hv + acc[i]);
-      }
+    for (int u = 0; u < kBatch; ++u) {
+      const int sp = sp0 + u;
+      const bool ok = sp < a.nsplit;
+      const size_t pr = sbase + (size_t)(ok ? sp : 0) * sstride;
+      mv[u] = ok ? a.part_m[pr] : kNegInf;
+      lv[u] = ok ? a.part_l[pr] : 0.f;
+      ov[u] = ok ? *reinterpret_cast<const f32x4*>(a.part_o + pr * D + d) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
+    // running merge: rescale what is accumulated to the new maximum
+    float Mb = M;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) Mb = fmaxf(Mb, mv[u]);
+    const float keep = M == kNegInf ? 0.f : __builtin_amdgcn_exp2f(M - Mb);
+    acc *= keep;
+    Ls *= keep;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const float e = mv[u] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mv[u] - Mb);
+      acc += ov[u] * e;
+      Ls += lv[u] * e;
+    }
+    M = Mb;
   }
+  const float inv = 1.f / Ls;
+  acc *= inv;
+  if (a.attn_out) *reinterpret_cast<f32x4*>(a.attn_out + gi) = acc;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) Elem<T>::store(a.x_out, gi + i, hv[i] + acc[i]);
 }
 
 template <typename T, int D>
@@ -674,6 +746,20 @@ hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int thre
   if (dtype == 0 && head_dim == 128) return launch_nb<float, 128>(nb, grid, threads, lds, a, s);
   if (dtype == 0 && head_dim == 64) return launch_nb<float, 64>(nb, grid, threads, lds, a, s);
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_attn_merge(int dtype, int head_dim, dim3 grid, const AttnArgs& a, hipStream_t s) {
+  if (dtype == 1 && head_dim == 128)
+    hipLaunchKernelGGL((attn_merge_kernel<bf16_t, 128>), grid, dim3(256), 0, s, a);
+  else if (dtype == 1 && head_dim == 64)
+    hipLaunchKernelGGL((attn_merge_kernel<bf16_t, 64>), grid, dim3(256), 0, s, a);
+  else if (dtype == 0 && head_dim == 128)
+    hipLaunchKernelGGL((attn_merge_kernel<float, 128>), grid, dim3(256), 0, s, a);
+  else if (dtype == 0 && head_dim == 64)
+    hipLaunchKernelGGL((attn_merge_kernel<float, 64>), grid, dim3(256), 0, s, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
 }
 
 hipError_t set_tree_attn_lds_limit(int dtype, int head_dim, int nb, size_t lds) {

@@ -146,9 +146,12 @@ struct RowStats {
   __device__ __forceinline__ void merge_level();
 };
 
-// Butterfly partner exchange at level 0..5 of a wave: levels 0-3 pair lanes
-// inside a 16-lane row with DPP moves (xor 1, xor 2, mirror within 8, mirror
-// within 16); levels 4 and 5 pair rows (xor 16, xor 32) with a lane shuffle.
+// Butterfly partner exchange at level 0..5 of a wave (all 64 lanes active):
+// levels 0-3 pair lanes inside a 16-lane row with DPP moves (xor 1, xor 2,
+// mirror within 8, mirror within 16); levels 4 and 5 pair rows (xor 16, xor 32)
+// with gfx950's v_permlane16_swap / v_permlane32_swap.  Swapping a register
+// with itself leaves, in the two results, each lane's own value and its
+// partner row's value; the lane picks the partner's.
 // After levels 0..L every lane holds the combination of its 2^(L+1) lanes.
 template <int LEVEL>
 __device__ __forceinline__ int xchg(int v) {
@@ -156,8 +159,13 @@ __device__ __forceinline__ int xchg(int v) {
   if constexpr (LEVEL == 1) return __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);   // quad_perm 2,3,0,1
   if constexpr (LEVEL == 2) return __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false);  // row_half_mirror
   if constexpr (LEVEL == 3) return __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, false);  // row_mirror
-  if constexpr (LEVEL == 4) return __shfl_xor(v, 16, 64);
-  return __shfl_xor(v, 32, 64);
+  const int lane = (int)(threadIdx.x & 63);
+  if constexpr (LEVEL == 4) {
+    const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);  // odd rows <-> even rows
+    return (lane & 16) ? (int)r[0] : (int)r[1];
+  }
+  const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);    // upper half <-> lower half
+  return (lane & 32) ? (int)r[0] : (int)r[1];
 }
 template <int LEVEL>
 __device__ __forceinline__ float xchg(float v) {

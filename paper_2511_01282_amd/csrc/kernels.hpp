@@ -19,16 +19,14 @@ struct AttnArgs {
   const int32_t* node_off; // [B+1]
   const int32_t* kv_len;   // [B]
   const int32_t* parent;   // [M]
-  float* part_o;           // [B*Hkv*n_rowblk][nsplit][rows_per_wg][D]
+  float* part_o;           // [B*Hkv*n_rowblk][nsplit][rows_per_wg][D] unnormalised split outputs
   float* part_m;           // [B*Hkv*n_rowblk][nsplit][rows_per_wg]   (log2 units)
   float* part_l;
-  int32_t* counter;        // [B*Hkv*n_rowblk]
   void* x_out;             // [M][Hd] residual h + O in the workload dtype
   float* attn_out;         // [M][Hd] or null
   int32_t total_nodes, hidden_size, n_kv_heads, group, kv_cap, max_nodes;
   int32_t nsplit, chunk, n_rowblk, rows_per_wg, wr, wk;
   float scale_log2;        // log2(e) / sqrt(D)
-  int32_t lds_work_bytes;  // bytes of the kernel's LDS work area (after the ancestor table)
 };
 
 struct LmArgs {
@@ -65,6 +63,7 @@ struct VocabArgs {
 hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int threads, size_t lds,
                             const AttnArgs& a, hipStream_t s);
 hipError_t set_tree_attn_lds_limit(int dtype, int head_dim, int nb, size_t lds);
+hipError_t launch_attn_merge(int dtype, int head_dim, dim3 grid, const AttnArgs& a, hipStream_t s);
 hipError_t launch_lmhead(int dtype, int mb, int ko, const LmArgs& a, hipStream_t s);
 constexpr int kLmTileRows = 64;  // vocabulary rows per LM-head workgroup (one statistics tile)
 hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s);

@@ -191,6 +191,11 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmArgs a) {
   const size_t row_bytes = (size_t)a.hidden_size * ES;
   const int n_steps = (int)(row_bytes / kLmChunkBytes);
 
+  // Each workgroup walks the K steps from its own starting step (wrapping
+  // around): workgroups that run at the same time then read different column
+  // ranges of their rows, which spreads the requests over the memory channels
+  // (rows are 8 KB apart, so equal column offsets would land on the same ones).
+  const int rot = vt % n_steps;
   const int v = vw + lr;
   const bool wok = v < a.vocab;
   const char* wrow = reinterpret_cast<const char*>(a.w) + (size_t)(wok ? v : 0) * row_bytes + lg * 16;
@@ -202,24 +207,25 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmArgs a) {
 
   u32x4 wa[kLmPieces], wb[kLmPieces];
   XStage<MB> xs;
-  w_load(wa, wrow, wok, 0);
-  if (n_steps > 1) w_load(wb, wrow, wok, kLmChunkBytes);
-  x_load<MB>(xs, xbase, row_bytes, m0, a.m_rows, 0);
+  auto step_of = [&](int c) { return c + rot < n_steps ? c + rot : c + rot - n_steps; };
+  w_load(wa, wrow, wok, (size_t)step_of(0) * kLmChunkBytes);
+  if (n_steps > 1) w_load(wb, wrow, wok, (size_t)step_of(1) * kLmChunkBytes);
+  x_load<MB>(xs, xbase, row_bytes, m0, a.m_rows, step_of(0));
   x_store<MB>(xs, sx[0]);
   __syncthreads();
 
   for (int c = 0; c < n_steps; c += 2) {
     // ---- step c: wa, sx[0] ----
-    if (c + 1 < n_steps) x_load<MB>(xs, xbase, row_bytes, m0, a.m_rows, c + 1);
+    if (c + 1 < n_steps) x_load<MB>(xs, xbase, row_bytes, m0, a.m_rows, step_of(c + 1));
     mma_step<T, MB>(acc, wa, sx[0], lr, lg);
-    if (c + 2 < n_steps) w_load(wa, wrow, wok, (size_t)(c + 2) * kLmChunkBytes);
+    if (c + 2 < n_steps) w_load(wa, wrow, wok, (size_t)step_of(c + 2) * kLmChunkBytes);
     if (c + 1 >= n_steps) break;
     x_store<MB>(xs, sx[1]);
     __syncthreads();
     // ---- step c+1: wb, sx[1] ----
-    if (c + 2 < n_steps) x_load<MB>(xs, xbase, row_bytes, m0, a.m_rows, c + 2);
+    if (c + 2 < n_steps) x_load<MB>(xs, xbase, row_bytes, m0, a.m_rows, step_of(c + 2));
     mma_step<T, MB>(acc, wb, sx[1], lr, lg);
-    if (c + 3 < n_steps) w_load(wb, wrow, wok, (size_t)(c + 3) * kLmChunkBytes);
+    if (c + 3 < n_steps) w_load(wb, wrow, wok, (size_t)step_of(c + 3) * kLmChunkBytes);
     if (c + 2 < n_steps) {
       x_store<MB>(xs, sx[0]);
       __syncthreads();
