@@ -10,10 +10,11 @@ length 2048, a 26-node random draft tree, bf16 with fp32 accumulation).
 Inputs are resident in HBM before timing starts.  Several copies of the large
 inputs (K/V cache, LM head, hidden states) are rotated from step to step so
 that the working set exceeds the 256 MB Infinity Cache and every step streams
-its bytes from HBM.  Per-stage HIP events are recorded on the step's stream
-inside the timed region; they give each kernel's average duration for the
-roofline figures.  The CPU baseline times the oracle on the host cores on a
-bounded sample of the same workload.
+its bytes from HBM.  The timed region runs K plain steps.  A second pass of K
+steps records HIP events on the step's stream around each stage (attention
+with its split merge, LM head, vocabulary pass); they give each stage's
+average duration for the roofline figures.  The CPU baseline times the oracle
+on the host cores on a bounded sample of the same workload.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
@@ -45,7 +46,11 @@ def stage_bytes(w, M, es):
     kv_rows = sum(int(w.kv_len[b]) + int(w.node_off[b + 1] - w.node_off[b]) for b in range(len(w.kv_len)))
     attn = 2 * s.n_kv_heads * kv_rows * s.head_dim * es + 2 * M * s.hidden * es   # K,V + h in + x out
     lm = s.vocab * s.hidden * es + M * s.hidden * es + M * s.vocab * 4            # W + x + logits out
-    vocab = M * s.vocab * 4                                                        # logits read once
+    # the LM-head epilogue reduces every 64-logit tile to a partial (m, S, T, argmax and
+    # the top-K keys, K = 8 or 16), so the vocabulary pass reads those, not the logits
+    n_vtiles = (s.vocab + 63) // 64
+    ko = 8 if s.topk_out <= 8 else 16
+    vocab = M * n_vtiles * (4 + 2 * ko) * 4 + M * 4                               # partials + child logits
     vis = 0
     for b in range(len(w.kv_len)):
         lo, hi = int(w.node_off[b]), int(w.node_off[b + 1])
@@ -67,8 +72,6 @@ def main():
     ap.add_argument("--rotate", type=int, default=0, help="input copies rotated per step (0: enough to exceed MALL)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-stage-events", action="store_true",
-                    help="time plain launches only (also reported with stage events otherwise)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -123,27 +126,26 @@ def main():
     torch.cuda.synchronize()
 
     K = args.steps
-    t_plain = None
-    if args.no_stage_events:
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for i in range(K):
-            plan.step(sets[i % R], out, stream=stream, **kw)
-        torch.cuda.synchronize()
-        t_plain = time.perf_counter() - t0
-        log(f"[bench] plain launches: {t_plain * 1e6 / K:.1f} us/step")
+    # timed region: K plain steps (no per-stage events), bracketed by synchronisations
+    torch.cuda.synchronize()
+    log(f"[bench] timing {K} steps")
+    t0 = time.perf_counter()
+    for i in range(K):
+        plan.step(sets[i % R], out, stream=stream, **kw)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / K
+
+    # per-stage durations: a second pass of K steps with HIP events recorded by the
+    # library on the step's stream before and after each stage
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
     for row in evs:
         for e in row:
             e.record(stream)
     torch.cuda.synchronize()
-    log(f"[bench] timing {K} steps")
-    t0 = time.perf_counter()
     for i in range(K):
         plan.step(sets[i % R], out, stream=stream, stage_events=evs[i], **kw)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_step = wall * 1e3 / K
 
     st = {"attn": [], "lm": [], "vocab": [], "step": []}
     for row in evs:

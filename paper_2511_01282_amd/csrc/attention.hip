@@ -29,6 +29,9 @@
 
 namespace respec {
 
+// Headroom of the lazily raised softmax reference maximum (log2 units).
+constexpr float kLazyMargin = 8.f;
+
 // Bit ai of a 128-bit ancestor set.
 __device__ __forceinline__ bool anc_has(const u32x4& w, int ai) {
   const uint32_t word = ai < 64 ? (ai < 32 ? w[0] : w[1]) : (ai < 96 ? w[2] : w[3]);
@@ -146,10 +149,15 @@ __device__ __forceinline__ void process_tile(const AttnTile<T, D>& t, int t0, in
     for (int kb = 0; kb < 2; ++kb) tm = fmaxf(tm, fmaxf(fmaxf(s[kb][nb][0], s[kb][nb][1]), fmaxf(s[kb][nb][2], s[kb][nb][3])));
     tm = fmaxf(tm, xchg<4>(tm));
     tm = fmaxf(tm, xchg<5>(tm));
-    const float mn = fmaxf(m_run[nb], tm * scale_log2);
-    const bool none = mn == kNegInf;
-    const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(m_run[nb] - mn);
-    const float mb = none ? 0.f : mn;
+    // m_run is a reference maximum: it is raised only when a score exceeds it by more
+    // than kLazyMargin (so p <= 2^kLazyMargin), and the accumulators are rescaled only
+    // then; while it is unset (-inf) the accumulators are zero and need no rescale.
+    const float tmax = tm * scale_log2;
+    const bool raise = tmax > m_run[nb] + kLazyMargin;
+    const float mn = raise ? tmax : m_run[nb];
+    const bool rescale = raise && m_run[nb] != kNegInf;
+    const float alpha = rescale ? __builtin_amdgcn_exp2f(m_run[nb] - mn) : 1.f;
+    const float mb = mn == kNegInf ? 0.f : mn;
     float ps = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -161,7 +169,7 @@ __device__ __forceinline__ void process_tile(const AttnTile<T, D>& t, int t0, in
       }
     l_run[nb] = l_run[nb] * alpha + ps;
     m_run[nb] = mn;
-    if (__any(alpha != 1.f)) {
+    if (__any(rescale)) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) o[db][nb] *= alpha;
     }
@@ -359,10 +367,15 @@ __device__ __forceinline__ void softmax_pv_bf16(f32x4 (&s)[2][NB], const u32x4 (
       tm = fmaxf(tm, fmaxf(fmaxf(s[kb][nb][0], s[kb][nb][1]), fmaxf(s[kb][nb][2], s[kb][nb][3])));
     tm = fmaxf(tm, xchg<4>(tm));
     tm = fmaxf(tm, xchg<5>(tm));
-    const float mn = fmaxf(m_run[nb], tm * scale_log2);
-    const bool none = mn == kNegInf;
-    const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(m_run[nb] - mn);
-    const float mb = none ? 0.f : mn;
+    // m_run is a reference maximum: it is raised only when a score exceeds it by more
+    // than kLazyMargin (so p <= 2^kLazyMargin), and the accumulators are rescaled only
+    // then; while it is unset (-inf) the accumulators are zero and need no rescale.
+    const float tmax = tm * scale_log2;
+    const bool raise = tmax > m_run[nb] + kLazyMargin;
+    const float mn = raise ? tmax : m_run[nb];
+    const bool rescale = raise && m_run[nb] != kNegInf;
+    const float alpha = rescale ? __builtin_amdgcn_exp2f(m_run[nb] - mn) : 1.f;
+    const float mb = mn == kNegInf ? 0.f : mn;
     float ps = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -374,7 +387,7 @@ __device__ __forceinline__ void softmax_pv_bf16(f32x4 (&s)[2][NB], const u32x4 (
       }
     l_run[nb] = l_run[nb] * alpha + ps;
     m_run[nb] = mn;
-    if (__any(alpha != 1.f)) {
+    if (__any(rescale)) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) o[db][nb] *= alpha;
     }
