@@ -93,17 +93,12 @@ respec_status respec_verify_create(const respec_verify_shape* shape, respec_veri
   p->es = es;
   p->group = s.n_q_heads / s.n_kv_heads;
 
-  // attention: rows of a KV head are (node, head-in-group) pairs
+  // attention: rows of a KV head are (node, head-in-group) pairs; a wave owns
+  // at most 32 of them (more would not fit the registers next to a ring of
+  // tiles); above 4 waves' worth a head's KV rows are read once per row block
   const int rmax = s.max_nodes * p->group;
-  int nb, rg;
-  if (rmax <= 64) {
-    nb = cdiv(rmax, 16);
-    rg = 1;
-  } else {
-    const int w3 = cdiv(rmax, 48) * 48 - rmax, w4 = cdiv(rmax, 64) * 64 - rmax;
-    nb = w3 < w4 ? 3 : 4;
-    rg = cdiv(rmax, 16 * nb);
-  }
+  const int nb = rmax <= 16 ? 1 : 2;
+  const int rg = cdiv(rmax, 16 * nb);
   p->nb = nb;
   p->wr = rg < 4 ? rg : 4;
   p->n_rowblk = cdiv(rg, p->wr);

@@ -732,8 +732,6 @@ static hipError_t launch_nb(int nb, dim3 grid, int threads, size_t lds, const At
   switch (nb) {
     case 1: hipLaunchKernelGGL((tree_attn_kernel<T, D, 1>), grid, dim3(threads), lds, s, a); break;
     case 2: hipLaunchKernelGGL((tree_attn_kernel<T, D, 2>), grid, dim3(threads), lds, s, a); break;
-    case 3: hipLaunchKernelGGL((tree_attn_kernel<T, D, 3>), grid, dim3(threads), lds, s, a); break;
-    case 4: hipLaunchKernelGGL((tree_attn_kernel<T, D, 4>), grid, dim3(threads), lds, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -745,8 +743,6 @@ static hipError_t set_lds_nb(int nb, size_t lds) {
   switch (nb) {
     case 1: f = reinterpret_cast<const void*>(&tree_attn_kernel<T, D, 1>); break;
     case 2: f = reinterpret_cast<const void*>(&tree_attn_kernel<T, D, 2>); break;
-    case 3: f = reinterpret_cast<const void*>(&tree_attn_kernel<T, D, 3>); break;
-    case 4: f = reinterpret_cast<const void*>(&tree_attn_kernel<T, D, 4>); break;
     default: return hipErrorInvalidValue;
   }
   return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
