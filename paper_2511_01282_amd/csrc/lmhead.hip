@@ -254,6 +254,214 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Tiled variant for many token rows (up to 256 per pass).  With many token
+// rows the x tile, not W, dominates what a workgroup pulls through its CU, so
+// a workgroup here owns 128 vocabulary rows (each x row it loads serves twice
+// as many W rows):
+//   - 4 waves in a 2 x 2 grid: wave (wv, wm) computes vocabulary rows
+//     64*wv .. +63 (four 16-row blocks, one statistics tile) against token rows
+//     16*MB*wm .. +16*MB-1;
+//   - K advances in 128-byte steps.  The W fragments and this thread's share
+//     of the x tile of step c+3 are requested together, right after step c's
+//     matrix products, so waiting for the oldest step (W and x of step c)
+//     never waits for the newer loads: steps c+1 and c+2 stay in flight.  x
+//     goes from registers to a double-buffered LDS tile (one barrier per
+//     step), from which every wave reads its B fragments;
+//   - each wave reduces its own 64 vocabulary rows to the per-tile statistics.
+constexpr int kTlStep = 128;                 // bytes of a row per K step
+constexpr int kTlPieces = kTlStep / 64;      // mma_k64 calls per K step
+constexpr int kTlXStride = kTlStep + 16;     // LDS row stride of the x tile
+constexpr int kTlRows = 128;                 // vocabulary rows per workgroup
+
+template <int MB, int KO>
+__global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
+  constexpr int VB = 4;                            // 16-row vocabulary blocks per wave
+  constexpr int MT = 32 * MB;                      // token rows per workgroup
+  constexpr int XP = MT * kTlStep / 16 / 256;      // 16-byte x pieces per thread per step
+  constexpr int W = TilePartial<KO>::kWords;
+  __shared__ __align__(16) unsigned char sx[2 * MT * kTlXStride];
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int wv = wave & 1, wm = wave >> 1;
+  const int n_mt = a.n_mtiles;
+  const int id = blockIdx.x;
+  const int grp = id / (8 * n_mt), rem = id % (8 * n_mt);
+  const int vt = grp * 8 + rem % 8, mt = rem / 8;  // vt: 128-row tile
+  if (vt * kTlRows >= a.vocab) return;
+  const int v0 = vt * kTlRows + 64 * wv;           // first vocabulary row of this wave
+  const int stat_tile = 2 * vt + wv;               // this wave's 64-row statistics tile
+  const int m0 = mt * MT;                          // first token row of the workgroup
+  const size_t row_bytes = (size_t)a.hidden_size * 2;
+  const int n_steps = (int)(row_bytes / kTlStep);  // >= 4 (hidden*2 is a multiple of 512)
+  const int rot = vt % n_steps;                    // per-workgroup K start (spreads the channels)
+  auto step_of = [&](int c) { return c + rot < n_steps ? c + rot : c + rot - n_steps; };
+
+  const char* wrow[VB];
+#pragma unroll
+  for (int vb = 0; vb < VB; ++vb) {
+    const int v = min(v0 + 16 * vb + lr, a.vocab - 1);  // rows past V: a valid row, results not stored
+    wrow[vb] = reinterpret_cast<const char*>(a.w) + (size_t)v * row_bytes + lg * 16;
+  }
+  const char* xbase = reinterpret_cast<const char*>(a.x);
+
+  struct Stage {
+    u32x4 w[VB][kTlPieces];
+    u32x4 x[XP];
+  };
+  auto issue = [&](Stage& st, int c) {
+    const size_t off = (size_t)step_of(c) * kTlStep;
+#pragma unroll
+    for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+      for (int kp = 0; kp < kTlPieces; ++kp) st.w[vb][kp] = ld16(wrow[vb] + off + kp * 64);
+#pragma unroll
+    for (int t = 0; t < XP; ++t) {
+      const int idx = threadIdx.x + 256 * t;
+      const int r = idx / (kTlStep / 16), pc = idx % (kTlStep / 16);
+      const int m = min(m0 + r, a.m_rows - 1);  // rows past M: a valid row, results not stored
+      st.x[t] = ld16(xbase + (size_t)m * row_bytes + off + pc * 16);
+    }
+  };
+  auto stage_x = [&](const Stage& st, unsigned char* buf) {
+#pragma unroll
+    for (int t = 0; t < XP; ++t) {
+      const int idx = threadIdx.x + 256 * t;
+      const int r = idx / (kTlStep / 16), pc = idx % (kTlStep / 16);
+      *reinterpret_cast<u32x4*>(buf + r * kTlXStride + pc * 16) = st.x[t];
+    }
+  };
+
+  f32x4 acc[VB][MB];
+#pragma unroll
+  for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[vb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto mma_step = [&](const Stage& st, const unsigned char* buf) {
+#pragma unroll
+    for (int kp = 0; kp < kTlPieces; ++kp) {
+      u32x4 xb[MB];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+        xb[mb] = *reinterpret_cast<const u32x4*>(buf + (MB * 16 * wm + 16 * mb + lr) * kTlXStride + kp * 64 + lg * 16);
+#pragma unroll
+      for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) acc[vb][mb] = mma_k64(bf16_t{}, st.w[vb][kp], xb[mb], acc[vb][mb]);
+    }
+  };
+
+  // three stages in a ring: step c is consumed while steps c+1 and c+2 are in
+  // flight; after its products step c+3 goes into the freed registers (past
+  // the end: step n_steps-1 again, unused).  x alternates between two LDS
+  // buffers (the barrier of step c+1 orders step c's reads before the writes
+  // of step c+2).
+  Stage s0, s1, s2;
+  issue(s0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  issue(s1, 1);
+  __builtin_amdgcn_sched_barrier(0);
+  issue(s2, 2);
+  __builtin_amdgcn_sched_barrier(0);
+  auto step = [&](Stage& st, int c) {
+    unsigned char* buf = sx + (c & 1) * MT * kTlXStride;
+    stage_x(st, buf);
+    __syncthreads();
+    mma_step(st, buf);
+    issue(st, min(c + 3, n_steps - 1));
+    __builtin_amdgcn_sched_barrier(0);  // keep the requests here, ahead of the next step's wait
+  };
+  int c = 0;
+  for (; c + 2 < n_steps; c += 3) {  // no exit inside the body: every path around the loop issues three steps
+    step(s0, c);
+    step(s1, c + 1);
+    step(s2, c + 2);
+  }
+  if (c < n_steps) {
+    step(s0, c);
+    if (c + 1 < n_steps) step(s1, c + 1);
+  }
+
+  // logits: lane holds z[m0 + 16*MB*wm + 16*mb + lr][v0 + 16*vb + 4*lg + i]
+  const bool vec_ok = (a.vocab & 3) == 0;
+#pragma unroll
+  for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int m = m0 + MB * 16 * wm + 16 * mb + lr;
+      const int vv = v0 + 16 * vb + 4 * lg;
+      if (m >= a.m_rows) continue;
+      float* dst = a.logits + (size_t)m * a.vocab + vv;
+      if (vec_ok && vv + 3 < a.vocab) {
+        *reinterpret_cast<f32x4*>(dst) = acc[vb][mb];
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (vv + i < a.vocab) dst[i] = acc[vb][mb][i];
+      }
+    }
+  if (!a.partials || v0 >= a.vocab) return;  // (a wave past V has no statistics tile)
+
+  // per-tile statistics of each token row over this wave's 64 logits
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    float mx = kNegInf;
+#pragma unroll
+    for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int col = v0 + 16 * vb + 4 * lg + i;
+        mx = col < a.vocab ? fmaxf(mx, acc[vb][mb][i]) : mx;
+      }
+    RowStats st;
+    st.init();
+    st.m = mx;
+    uint64_t key[KO];
+#pragma unroll
+    for (int i = 0; i < KO; ++i) key[i] = 0ull;
+#pragma unroll
+    for (int vb = 0; vb < VB; ++vb) {
+      uint64_t kb[KO];
+#pragma unroll
+      for (int i = 0; i < KO; ++i) kb[i] = 0ull;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int col = v0 + 16 * vb + 4 * lg + i;
+        const bool ok = col < a.vocab;
+        const float d = acc[vb][mb][i] - mx;
+        const float e = ok ? __expf(d) : 0.f;
+        st.S += e;
+        st.T += ok ? e * d : 0.f;
+        st.am = (ok && acc[vb][mb][i] == mx) ? min(st.am, col) : st.am;
+        kb[i] = ok ? make_key(acc[vb][mb][i], col) : 0ull;
+      }
+      // sort this block's 4 keys, then merge them into the lane's list
+      auto cas = [&](int x, int y) {
+        const bool sw = kb[y] > kb[x];
+        const uint64_t kx = kb[x], ky = kb[y];
+        kb[x] = sw ? ky : kx;
+        kb[y] = sw ? kx : ky;
+      };
+      cas(0, 1); cas(2, 3); cas(0, 2); cas(1, 3); cas(1, 2);
+      merge_topk<KO>(key, kb);
+    }
+    st.merge_level<4>();  // lane groups of a token row: xor 16, xor 32
+    merge_topk_level<KO, 4>(key);
+    st.merge_level<5>();
+    merge_topk_level<KO, 5>(key);
+    const int m = m0 + MB * 16 * wm + 16 * mb + lr;
+    if (lg == 0 && m < a.m_rows) {
+      u32x4* dst = reinterpret_cast<u32x4*>(a.partials + ((size_t)m * a.n_vtiles + stat_tile) * W);
+      dst[0] = u32x4{__float_as_uint(st.m), __float_as_uint(st.S), __float_as_uint(st.T), (uint32_t)st.am};
+#pragma unroll
+      for (int i = 0; i < KO; i += 2)
+        dst[1 + i / 2] = u32x4{(uint32_t)key[i], (uint32_t)(key[i] >> 32), (uint32_t)key[i + 1],
+                               (uint32_t)(key[i + 1] >> 32)};
+    }
+  }
+}
+
 template <typename T, int KO>
 static hipError_t launch_mb(int mb, dim3 grid, const LmArgs& a, hipStream_t s) {
   switch (mb) {
@@ -270,6 +478,22 @@ hipError_t launch_lmhead(int dtype, int mb, int ko, const LmArgs& a, hipStream_t
   const int n_vt = (a.vocab + kLmRows - 1) / kLmRows;
   const int n_grp = (n_vt + 7) / 8;
   dim3 grid(n_grp * 8 * a.n_mtiles);
+  if (mb == 8 || mb == 16) {  // tiled variant: MT = 128 or 256 token rows, 128-row vocabulary tiles (bf16)
+    if (dtype != 1) return hipErrorInvalidValue;
+    const int n_vt2 = (a.vocab + kTlRows - 1) / kTlRows;
+    dim3 tgrid(((n_vt2 + 7) / 8) * 8 * a.n_mtiles);
+    const int tmb = mb / 2;
+    if (ko == 8) {
+      if (tmb == 4) hipLaunchKernelGGL((lmhead_tiled_kernel<4, 8>), tgrid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((lmhead_tiled_kernel<8, 8>), tgrid, dim3(256), 0, s, a);
+    } else if (ko == 16) {
+      if (tmb == 4) hipLaunchKernelGGL((lmhead_tiled_kernel<4, 16>), tgrid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((lmhead_tiled_kernel<8, 16>), tgrid, dim3(256), 0, s, a);
+    } else {
+      return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   if (ko == 8) return dtype == 1 ? launch_mb<bf16_t, 8>(mb, grid, a, s) : launch_mb<float, 8>(mb, grid, a, s);
   if (ko == 16) return dtype == 1 ? launch_mb<bf16_t, 16>(mb, grid, a, s) : launch_mb<float, 16>(mb, grid, a, s);
   return hipErrorInvalidValue;
