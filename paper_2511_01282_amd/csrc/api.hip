@@ -19,6 +19,8 @@ struct respec_verify_plan {
   int group;              // Hq / Hkv
   // attention tiling
   int nb, wr, wk, rows_per_wg, n_rowblk, attn_threads, nsplit_cap;
+  int attn_shared;        // bf16 with several waves of rows per KV head: KV tiles shared through LDS
+  int attn_wg_target;     // workgroups the splits aim for
   size_t attn_lds;
   // vocabulary statistics: tiles of the LM head and top-K list length
   int ko, n_vtiles;
@@ -32,6 +34,7 @@ struct respec_verify_plan {
 namespace {
 
 constexpr int kTargetWaves = 1024;  // attention: one wave per SIMD on a 256-CU MI355X
+constexpr int kCUs = 256;
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
@@ -99,24 +102,39 @@ respec_status respec_verify_create(const respec_verify_shape* shape, respec_veri
   const int rmax = s.max_nodes * p->group;
   const int nb = rmax <= 16 ? 1 : 2;
   const int rg = cdiv(rmax, 16 * nb);
-  p->nb = nb;
-  p->wr = rg < 4 ? rg : 4;
-  p->n_rowblk = cdiv(rg, p->wr);
   const int rb = 16 * nb;
-  int wk = 4 / p->wr;
-  if (wk > 128 / (p->wr * rb)) wk = 128 / (p->wr * rb);
-  p->wk = wk < 1 ? 1 : wk;
-  p->rows_per_wg = p->wr * rb;
-  const int nwaves = p->wr * p->wk;
-  p->attn_threads = 64 * nwaves;
-  // per wave: one row-major, swizzled V tile (bf16) or one transposed, padded V tile (float32)
-  const size_t vt_bytes = es == 2 ? (size_t)nwaves * kKvTile * s.head_dim * es
-                                  : (size_t)nwaves * s.head_dim * (kKvTile + kVtPad) * es;
-  const size_t merge_bytes = p->wk > 1 ? ((size_t)nwaves * rb * (s.head_dim + 2) + (size_t)p->wr * rb) * 4 : 0;
   const long long t_cap = (long long)s.max_kv_len + s.max_nodes;
+  p->nb = nb;
+  p->attn_shared = es == 2 && rg >= 2;
+  if (p->attn_shared) {
+    // up to 8 waves of rows read every KV tile once, from a shared LDS ring; a
+    // workgroup of more than 4 such waves fills a CU (two waves per SIMD)
+    p->wr = rg < 8 ? rg : 8;
+    p->n_rowblk = cdiv(rg, p->wr);
+    p->wk = 1;
+    p->rows_per_wg = p->wr * rb;
+    p->attn_threads = 64 * p->wr;
+    p->attn_lds = (size_t)kShRingBytesPerD * s.head_dim;
+    p->attn_wg_target = kCUs * (p->wr <= 4 ? 2 : 1);
+  } else {
+    p->wr = rg < 4 ? rg : 4;
+    p->n_rowblk = cdiv(rg, p->wr);
+    int wk = 4 / p->wr;
+    if (wk > 128 / (p->wr * rb)) wk = 128 / (p->wr * rb);
+    p->wk = wk < 1 ? 1 : wk;
+    p->rows_per_wg = p->wr * rb;
+    const int nwaves = p->wr * p->wk;
+    p->attn_threads = 64 * nwaves;
+    // per wave: one row-major, swizzled V tile (bf16) or one transposed, padded V tile (float32)
+    const size_t vt_bytes = es == 2 ? (size_t)nwaves * kKvTile * s.head_dim * es
+                                    : (size_t)nwaves * s.head_dim * (kKvTile + kVtPad) * es;
+    const size_t merge_bytes =
+        p->wk > 1 ? ((size_t)nwaves * rb * (s.head_dim + 2) + (size_t)p->wr * rb) * 4 : 0;
+    p->attn_lds = vt_bytes > merge_bytes ? vt_bytes : merge_bytes;
+    p->attn_wg_target = kTargetWaves / nwaves;
+  }
   const int per_split = s.n_kv_heads * p->n_rowblk;
-  p->nsplit_cap = clampi(kTargetWaves / (nwaves * per_split), 1, cdiv(t_cap, kKvTile));
-  p->attn_lds = vt_bytes > merge_bytes ? vt_bytes : merge_bytes;
+  p->nsplit_cap = clampi(p->attn_wg_target / per_split, 1, cdiv(t_cap, kKvTile));
 
   p->ko = s.topk_out <= 8 ? 8 : 16;
   p->n_vtiles = cdiv(s.vocab, kLmTileRows);
@@ -195,7 +213,9 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   int32_t* cnt = reinterpret_cast<int32_t*>(ws + plan->off_cnt);
 
   if (!plan->lds_ready.load(std::memory_order_acquire)) {
-    if (set_tree_attn_lds_limit(s.dtype, s.head_dim, plan->nb, plan->attn_lds) != hipSuccess) return RESPEC_ERR_HIP;
+    const hipError_t e = plan->attn_shared ? set_tree_attn_shared_lds_limit(s.head_dim, plan->nb, plan->attn_lds)
+                                           : set_tree_attn_lds_limit(s.dtype, s.head_dim, plan->nb, plan->attn_lds);
+    if (e != hipSuccess) return RESPEC_ERR_HIP;
     plan->lds_ready.store(true, std::memory_order_release);
   }
   if (ev && hipEventRecord(ev[0], st) != hipSuccess) return RESPEC_ERR_HIP;
@@ -221,7 +241,7 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   at.max_nodes = a.max_nodes_in_batch;
   const long long t_max = (long long)a.max_kv_len_in_batch + a.max_nodes_in_batch;
   const int per_split = a.batch * s.n_kv_heads * plan->n_rowblk;
-  const int target = clampi(kTargetWaves / (plan->attn_threads / 64 * per_split), 1, plan->nsplit_cap);
+  const int target = clampi(plan->attn_wg_target / per_split, 1, plan->nsplit_cap);
   at.chunk = cdiv(cdiv(t_max, target), kKvTile) * kKvTile;
   at.nsplit = cdiv(t_max, at.chunk);
   at.n_rowblk = plan->n_rowblk;
@@ -230,9 +250,11 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   at.wk = plan->wk;
   at.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.head_dim));
   dim3 agrid(at.nsplit, s.n_kv_heads * plan->n_rowblk, a.batch);
-  if (launch_tree_attn(s.dtype, s.head_dim, plan->nb, agrid, plan->attn_threads, plan->attn_lds, at, st) !=
-      hipSuccess)
-    return RESPEC_ERR_HIP;
+  const hipError_t ae =
+      plan->attn_shared
+          ? launch_tree_attn_shared(s.head_dim, plan->nb, agrid, plan->attn_threads, plan->attn_lds, at, st)
+          : launch_tree_attn(s.dtype, s.head_dim, plan->nb, agrid, plan->attn_threads, plan->attn_lds, at, st);
+  if (ae != hipSuccess) return RESPEC_ERR_HIP;
   const int merge_rows = 256 / (s.head_dim / 4);
   dim3 mgrid(cdiv(plan->rows_per_wg, merge_rows), a.batch * s.n_kv_heads * plan->n_rowblk);
   if (launch_attn_merge(s.dtype, s.head_dim, mgrid, at, st) != hipSuccess) return RESPEC_ERR_HIP;

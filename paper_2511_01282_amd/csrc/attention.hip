@@ -24,6 +24,8 @@
 //     x = round(h + O) (one workgroup alone cannot pull the partials of a
 //     head fast enough: a single CU's memory parallelism caps it at tens of
 //     GB/s).
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -332,13 +334,14 @@ __device__ __forceinline__ void read_vt_bf16(const unsigned char* vtile, int lan
   }
 }
 
-// Tree / range mask, online softmax and O^T += V^T P^T for one tile whose
-// scores are in s and whose V^T fragments are in vf.
+// Tree / range mask and online softmax of one tile whose scores are in s; the
+// accumulators are rescaled when the reference maximum rises, and the
+// probabilities come back as the hi + lo bf16 parts of the P^T fragments.
 template <int D, int NB>
-__device__ __forceinline__ void softmax_pv_bf16(f32x4 (&s)[2][NB], const u32x4 (&vf)[D / 16], int t0, int kv_hi,
-                                                int L, const int (&qnode)[NB], const u32x4 (&anc)[NB],
-                                                float scale_log2, float (&m_run)[NB], float (&l_run)[NB],
-                                                f32x4 (&o)[D / 16][NB], int lane) {
+__device__ __forceinline__ void softmax_p_bf16(f32x4 (&s)[2][NB], int t0, int kv_hi, int L, const int (&qnode)[NB],
+                                               const u32x4 (&anc)[NB], float scale_log2, float (&m_run)[NB],
+                                               float (&l_run)[NB], f32x4 (&o)[D / 16][NB], int lane,
+                                               u32x4 (&phi)[NB], u32x4 (&plo)[NB]) {
   constexpr int DB = D / 16;
   const int lg = lane >> 4;
   typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -393,7 +396,6 @@ __device__ __forceinline__ void softmax_pv_bf16(f32x4 (&s)[2][NB], const u32x4 (
     }
   }
   // P^T fragments, hi + lo bf16 parts
-  u32x4 phi[NB], plo[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
@@ -405,14 +407,32 @@ __device__ __forceinline__ void softmax_pv_bf16(f32x4 (&s)[2][NB], const u32x4 (
       plo[nb][j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{r0, r1}, bf16x2));
     }
   }
+}
+
+// O^T += V^T P^T for the output blocks db0 .. db0 + N - 1 (vf[j] holds block db0 + j).
+template <int D, int NB, int N>
+__device__ __forceinline__ void pv_bf16(const u32x4 (&vf)[N], int db0, const u32x4 (&phi)[NB],
+                                        const u32x4 (&plo)[NB], f32x4 (&o)[D / 16][NB]) {
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
+  for (int j = 0; j < N; ++j) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      o[db][nb] = mma_k64(bf16_t{}, vf[db], phi[nb], o[db][nb]);
-      o[db][nb] = mma_k64(bf16_t{}, vf[db], plo[nb], o[db][nb]);
+      o[db0 + j][nb] = mma_k64(bf16_t{}, vf[j], phi[nb], o[db0 + j][nb]);
+      o[db0 + j][nb] = mma_k64(bf16_t{}, vf[j], plo[nb], o[db0 + j][nb]);
     }
   }
+}
+
+// Mask, online softmax and O^T += V^T P^T for one tile whose scores are in s
+// and whose V^T fragments are in vf.
+template <int D, int NB>
+__device__ __forceinline__ void softmax_pv_bf16(f32x4 (&s)[2][NB], const u32x4 (&vf)[D / 16], int t0, int kv_hi,
+                                                int L, const int (&qnode)[NB], const u32x4 (&anc)[NB],
+                                                float scale_log2, float (&m_run)[NB], float (&l_run)[NB],
+                                                f32x4 (&o)[D / 16][NB], int lane) {
+  u32x4 phi[NB], plo[NB];
+  softmax_p_bf16<D, NB>(s, t0, kv_hi, L, qnode, anc, scale_log2, m_run, l_run, o, lane, phi, plo);
+  pv_bf16<D, NB, D / 16>(vf, 0, phi, plo, o);
 }
 
 // Ancestor-or-self bitsets of each lane's query nodes, walked up the parent
@@ -658,6 +678,288 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Shared-tile variant (bf16; a KV head's query rows span 2-8 waves).  Every
+// wave of such a workgroup needs the same KV rows, so each KV tile is fetched
+// once per workgroup, straight into LDS by DMA (global_load_lds, 16 bytes per
+// lane), into a ring of kShStages slots:
+//   - wave 0 requests the K half and wave 1 the V half of every tile;
+//   - tile i is consumed while tiles i+1 .. i+3 are in flight: a requesting
+//     wave waits until only its two newest tiles are pending, then one barrier
+//     publishes tile i to every wave and, as every wave has finished tile i-1
+//     by then, frees that slot for tile i+3, requested right after;
+//   - K fragments (A operand of S^T = K Q^T) and transposed V fragments are
+//     read from LDS by hand-issued DS instructions that carry their own wait.
+//     The compiler does not see these reads, so it does not make them wait for
+//     every DMA in flight (it cannot tell the ring slots apart);
+//   - each wave owns 16*NB query rows of its own: no cross-wave merge.
+// K slot layout: 32 rows x D bf16, chunk c of row r at chunk position
+// c ^ kswz(r), so that a quarter-wave reading one chunk column of 16 rows hits
+// 64 distinct banks; V slots use the layout of the register path (vswz).
+constexpr int kShStages = 4;
+
+template <int D>
+__device__ __forceinline__ int kswz(int r) {
+  return D == 128 ? (r & 15) : ((r >> 1) & 7);
+}
+
+// Request one half (K or V) of a 32-row tile into an LDS slot; rows at or past
+// kv_hi are clamped to kv_hi - 1 (masked, or weighted by zero, as above).
+template <int D, bool V>
+__device__ __forceinline__ void dma_half(unsigned char* slot, const char* base, int t0, int kv_hi, int lane) {
+  constexpr int CPR = D * 2 / 16;  // 16-byte chunks per row
+  constexpr int RPI = 64 / CPR;    // rows per DMA instruction (1 KB)
+#pragma unroll
+  for (int q = 0; q < kKvTile / RPI; ++q) {
+    const int r = q * RPI + lane / CPR, pos = lane % CPR;
+    const int p = min(t0 + r, kv_hi - 1);
+    const int c = pos ^ (V ? vswz<D>(r) : kswz<D>(r));  // chunk that belongs at position pos
+    __builtin_amdgcn_global_load_lds(
+        (const __attribute__((address_space(1))) void*)(base + (size_t)p * D * 2 + c * 16),
+        (__attribute__((address_space(3))) void*)(slot + q * 1024), 16, 0, 0);
+  }
+}
+
+// K fragments of rows 16*kb .. 16*kb+15 of the slot at LDS byte offset OFF
+// (OFF includes kb): kf[kc] = K[row 16*kb + lr][bytes 64*kc + 16*lg .. +15].
+template <int D, int OFF>
+__device__ __forceinline__ void lds_k_half(uint32_t lds0, int lane, u32x4 (&kf)[D * 2 / 64]) {
+  constexpr int KCH = D * 2 / 64;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int sw = kswz<D>(lr);  // kswz(16 + lr) == kswz(lr)
+  uint32_t ad[KCH];
+#pragma unroll
+  for (int kc = 0; kc < KCH; ++kc) ad[kc] = lds0 + lr * D * 2 + (((4 * kc + lg) ^ sw) << 4);
+  if constexpr (D == 128) {
+    asm volatile(
+        "ds_read_b128 %0, %4 offset:%8\n\t"
+        "ds_read_b128 %1, %5 offset:%8\n\t"
+        "ds_read_b128 %2, %6 offset:%8\n\t"
+        "ds_read_b128 %3, %7 offset:%8\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(kf[0]), "=&v"(kf[1]), "=&v"(kf[2]), "=&v"(kf[3])
+        : "v"(ad[0]), "v"(ad[1]), "v"(ad[2]), "v"(ad[3]), "n"(OFF)
+        : "memory");
+  } else {
+    asm volatile(
+        "ds_read_b128 %0, %2 offset:%4\n\t"
+        "ds_read_b128 %1, %3 offset:%4\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(kf[0]), "=&v"(kf[1])
+        : "v"(ad[0]), "v"(ad[1]), "n"(OFF)
+        : "memory");
+  }
+}
+
+// Transposed V fragments of output blocks db0 .. db0 + D/32 - 1 of the slot at
+// LDS byte offset OFF, as read_vt_bf16 (vf[j] holds block db0 + j).
+template <int D, int OFF>
+__device__ __forceinline__ void lds_vt_half(uint32_t lds0, int lane, int db0, u32x4 (&vf)[D / 32]) {
+  constexpr int N = D / 32;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int r = 4 * lg + lr / 4;
+  const int sw = vswz<D>(r);
+  uint32_t ad[N];
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    const int col = 16 * (db0 + j) + 4 * (lr % 4);
+    ad[j] = lds0 + r * (D * 2) + (((col >> 3) ^ sw) << 4) + (col & 7) * 2;
+  }
+  u32x2 h0[N], h1[N];
+  if constexpr (D == 128) {
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %8 offset:%12\n\t"
+        "ds_read_b64_tr_b16 %4, %8 offset:%13\n\t"
+        "ds_read_b64_tr_b16 %1, %9 offset:%12\n\t"
+        "ds_read_b64_tr_b16 %5, %9 offset:%13\n\t"
+        "ds_read_b64_tr_b16 %2, %10 offset:%12\n\t"
+        "ds_read_b64_tr_b16 %6, %10 offset:%13\n\t"
+        "ds_read_b64_tr_b16 %3, %11 offset:%12\n\t"
+        "ds_read_b64_tr_b16 %7, %11 offset:%13\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(h0[0]), "=&v"(h0[1]), "=&v"(h0[2]), "=&v"(h0[3]), "=&v"(h1[0]), "=&v"(h1[1]), "=&v"(h1[2]),
+          "=&v"(h1[3])
+        : "v"(ad[0]), "v"(ad[1]), "v"(ad[2]), "v"(ad[3]), "n"(OFF), "n"(OFF + 16 * D * 2)
+        : "memory");
+  } else {
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %4 offset:%6\n\t"
+        "ds_read_b64_tr_b16 %2, %4 offset:%7\n\t"
+        "ds_read_b64_tr_b16 %1, %5 offset:%6\n\t"
+        "ds_read_b64_tr_b16 %3, %5 offset:%7\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(h0[0]), "=&v"(h0[1]), "=&v"(h1[0]), "=&v"(h1[1])
+        : "v"(ad[0]), "v"(ad[1]), "n"(OFF), "n"(OFF + 16 * D * 2)
+        : "memory");
+  }
+#pragma unroll
+  for (int j = 0; j < N; ++j) vf[j] = u32x4{h0[j].x, h0[j].y, h1[j].x, h1[j].y};
+}
+
+template <int D, int NB>
+__global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
+  constexpr int KCH = D * 2 / 64;
+  constexpr int DB = D / 16;
+  constexpr int RB = 16 * NB;
+  constexpr int kTile = kKvTile * D * 2;  // bytes of one K or V half-tile
+  constexpr int kStage = 2 * kTile;
+  constexpr int kLpt = kTile / 1024;      // DMA instructions per half-tile
+  static_assert((kShStages - 1) * kStage + kTile + 16 * D * 2 < 65536, "DS offsets are 16-bit");
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)smem;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lr = lane & 15, lg = lane >> 4;
+  const int b = blockIdx.z;
+  const int g = blockIdx.y / a.n_rowblk, rb = blockIdx.y % a.n_rowblk;
+  const int split = blockIdx.x;
+
+  const int node0 = a.node_off[b], node1 = a.node_off[b + 1];
+  int n_nodes = node1 - node0;
+  if (node0 < 0 || node1 > a.total_nodes || n_nodes < 1 || n_nodes > a.max_nodes) n_nodes = 0;
+  int L = a.kv_len[b];
+  L = max(0, min(L, a.kv_cap - n_nodes));
+  const int R = n_nodes * a.group;
+  const int row_wg = rb * a.rows_per_wg;
+  if (row_wg >= R) return;  // uniform over the workgroup
+
+  const size_t head_row0 = ((size_t)b * a.n_kv_heads + g) * (size_t)a.kv_cap;
+  const char* kbase = reinterpret_cast<const char*>(a.k_cache) + head_row0 * D * 2;
+  const char* vbase = reinterpret_cast<const char*>(a.v_cache) + head_row0 * D * 2;
+  const int t_rows = L + n_nodes;
+  const int kv_lo = split * a.chunk;
+  const int kv_hi = min(kv_lo + a.chunk, t_rows);
+  const int n_tiles = kv_lo < kv_hi ? (kv_hi - kv_lo + kKvTile - 1) / kKvTile : 0;
+  const int t_last = max(kv_hi - 1, 0);
+  auto tile_row = [&](int i) { return i < n_tiles ? kv_lo + i * kKvTile : t_last; };
+
+  const int p_lo = a.parent[node0 + min(lane, n_nodes - 1)];
+  const int p_hi = a.parent[node0 + min(lane + 64, n_nodes - 1)];
+  const int row_wave = row_wg + wave * RB;
+  u32x4 qf[NB][KCH];
+  int qnode[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int r = row_wave + 16 * nb + lr;
+    const bool live = r < R;
+    const int rc = live ? r : 0;
+    const int node = rc / a.group;
+    const int h = g * a.group + (rc - node * a.group);
+    qnode[nb] = live ? node : -1;
+    const char* src = reinterpret_cast<const char*>(a.hidden) +
+                      ((size_t)(node0 + node) * a.hidden_size + (size_t)h * D) * 2;
+#pragma unroll
+    for (int kc = 0; kc < KCH; ++kc) {
+      const u32x4 v = ld16(src + kc * 64 + lg * 16);
+      qf[nb][kc] = live ? v : u32x4{0, 0, 0, 0};
+    }
+  }
+
+  // the first kShStages - 1 tiles (kv_hi >= 1, so every clamped row is a valid cache row)
+  if (wave < 2) {
+#pragma unroll
+    for (int st = 0; st < kShStages - 1; ++st) {
+      if (wave == 0)
+        dma_half<D, false>(smem + st * kStage, kbase, tile_row(st), kv_hi, lane);
+      else
+        dma_half<D, true>(smem + st * kStage + kTile, vbase, tile_row(st), kv_hi, lane);
+    }
+  }
+
+  float m_run[NB], l_run[NB];
+  f32x4 o[DB][NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    m_run[nb] = kNegInf;
+    l_run[nb] = 0.f;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[db][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  u32x4 anc[NB];
+  ancestor_bits<NB>(qnode, p_lo, p_hi, n_nodes, anc);
+
+  auto tile_step = [&](auto stage, int i) {
+    constexpr int S = decltype(stage)::value;
+    constexpr int kSlot = S * kStage;
+    constexpr int kNext = ((S + kShStages - 1) % kShStages) * kStage;  // slot of tile i-1, refilled with i+3
+    if (wave < 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((kShStages - 2) * kLpt) : "memory");
+    __builtin_amdgcn_s_barrier();
+    if (wave == 0)
+      dma_half<D, false>(smem + kNext, kbase, tile_row(i + kShStages - 1), kv_hi, lane);
+    else if (wave == 1)
+      dma_half<D, true>(smem + kNext + kTile, vbase, tile_row(i + kShStages - 1), kv_hi, lane);
+    // scores, one 16-row half of the tile at a time (fewer live registers)
+    f32x4 s[2][NB];
+    {
+      u32x4 kf[KCH];
+      lds_k_half<D, kSlot>(lds0, lane, kf);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < KCH; ++kc) acc = mma_k64(bf16_t{}, kf[kc], qf[nb][kc], acc);
+        s[0][nb] = acc;
+      }
+      lds_k_half<D, kSlot + 16 * D * 2>(lds0, lane, kf);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < KCH; ++kc) acc = mma_k64(bf16_t{}, kf[kc], qf[nb][kc], acc);
+        s[1][nb] = acc;
+      }
+    }
+    u32x4 phi[NB], plo[NB];
+    softmax_p_bf16<D, NB>(s, kv_lo + i * kKvTile, kv_hi, L, qnode, anc, a.scale_log2, m_run, l_run, o, lane, phi,
+                          plo);
+    // O^T += V^T P^T, half of the output blocks at a time
+    u32x4 vf[DB / 2];
+    lds_vt_half<D, kSlot + kTile>(lds0, lane, 0, vf);
+    pv_bf16<D, NB, DB / 2>(vf, 0, phi, plo, o);
+    lds_vt_half<D, kSlot + kTile>(lds0, lane, DB / 2, vf);
+    pv_bf16<D, NB, DB / 2>(vf, DB / 2, phi, plo, o);
+  };
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  using S3 = std::integral_constant<int, 3>;
+  static_assert(kShStages == 4, "the loop below walks four slots");
+  int i = 0;
+  for (; i + 3 < n_tiles; i += 4) {
+    tile_step(S0{}, i);
+    tile_step(S1{}, i + 1);
+    tile_step(S2{}, i + 2);
+    tile_step(S3{}, i + 3);
+  }
+  if (i < n_tiles) tile_step(S0{}, i);
+  if (i + 1 < n_tiles) tile_step(S1{}, i + 1);
+  if (i + 2 < n_tiles) tile_step(S2{}, i + 2);
+  // the DMAs past the last tile must land before the workgroup's LDS is released
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    l_run[nb] += xchg<4>(l_run[nb]);
+    l_run[nb] += xchg<5>(l_run[nb]);
+  }
+  const int bgr = (b * a.n_kv_heads + g) * a.n_rowblk + rb;
+  const size_t pbase = ((size_t)bgr * a.nsplit + split) * a.rows_per_wg;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int rl = wave * RB + 16 * nb + lr;
+    if (row_wg + rl >= R) continue;  // rows past the group's last are never merged
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+      *reinterpret_cast<f32x4*>(a.part_o + (pbase + rl) * D + 16 * db + 4 * lg) = o[db][nb];
+    if (lg == 0) {
+      a.part_m[pbase + rl] = m_run[nb];
+      a.part_l[pbase + rl] = l_run[nb];
+    }
+  }
+}
+
 // Split merge and residual: one workgroup per (sequence, KV head, row block,
 // chunk of 256 / (D/4) rows); each thread owns one (row, 4-column) item and
 // requests the partials, maxima and sums of 8 splits at a time.
@@ -754,6 +1056,38 @@ hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int thre
   if (dtype == 1 && head_dim == 64) return launch_nb<bf16_t, 64>(nb, grid, threads, lds, a, s);
   if (dtype == 0 && head_dim == 128) return launch_nb<float, 128>(nb, grid, threads, lds, a, s);
   if (dtype == 0 && head_dim == 64) return launch_nb<float, 64>(nb, grid, threads, lds, a, s);
+  return hipErrorInvalidValue;
+}
+
+template <int D>
+static hipError_t shared_nb(int nb, bool launch, dim3 grid, int threads, size_t lds, const AttnArgs& a,
+                            hipStream_t s) {
+  const void* f = nullptr;
+  switch (nb) {
+    case 1: f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 1>); break;
+    case 2: f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2>); break;
+    default: return hipErrorInvalidValue;
+  }
+  if (!launch) return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (nb == 1)
+    hipLaunchKernelGGL((tree_attn_shared_kernel<D, 1>), grid, dim3(threads), lds, s, a);
+  else
+    hipLaunchKernelGGL((tree_attn_shared_kernel<D, 2>), grid, dim3(threads), lds, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_tree_attn_shared(int head_dim, int nb, dim3 grid, int threads, size_t lds, const AttnArgs& a,
+                                   hipStream_t s) {
+  if (threads < 128 || threads > 512 || threads % 64) return hipErrorInvalidValue;  // 2..8 waves
+  if (head_dim == 128) return shared_nb<128>(nb, true, grid, threads, lds, a, s);
+  if (head_dim == 64) return shared_nb<64>(nb, true, grid, threads, lds, a, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t set_tree_attn_shared_lds_limit(int head_dim, int nb, size_t lds) {
+  const AttnArgs none{};
+  if (head_dim == 128) return shared_nb<128>(nb, false, dim3(), 0, lds, none, nullptr);
+  if (head_dim == 64) return shared_nb<64>(nb, false, dim3(), 0, lds, none, nullptr);
   return hipErrorInvalidValue;
 }
 

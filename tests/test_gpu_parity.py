@@ -102,6 +102,8 @@ EDGE = {
     "chain-causal-f32": ("f32", 2, 1, 64, [[-1] + list(range(0, 20))], [45]),
     "gqa8-star": ("bf16", 8, 1, 128, [[-1] + [0] * 30], [130]),
     "d64-bf16-mixed": ("bf16", 4, 4, 64, [[-1, 0, 1, 2, 0, 4, 5, 1, 7]], [64]),
+    # 96 query rows per KV head (three waves sharing each KV tile), head_dim 64
+    "d64-bf16-shared-rows": ("bf16", 4, 2, 64, [[-1] + [j // 2 for j in range(0, 47)]], [300]),
     "max-nodes-128": ("bf16", 2, 2, 128, [[-1] + [max(0, j - 4) for j in range(1, 128)]], [31]),
     "max-depth-64": ("bf16", 2, 2, 128, [[-1] + list(range(0, 64))], [5]),
 }
