@@ -20,6 +20,7 @@ struct respec_verify_plan {
   // attention tiling
   int nb, wr, wk, rows_per_wg, n_rowblk, attn_threads, nsplit_cap;
   int attn_shared;        // bf16 with several waves of rows per KV head: KV tiles shared through LDS
+  int attn_stages;        // ring slots of the shared-tile kernel
   int attn_wg_target;     // workgroups the splits aim for
   size_t attn_lds;
   // vocabulary statistics: tiles of the LM head and top-K list length
@@ -114,7 +115,9 @@ respec_status respec_verify_create(const respec_verify_shape* shape, respec_veri
     p->wk = 1;
     p->rows_per_wg = p->wr * rb;
     p->attn_threads = 64 * p->wr;
-    p->attn_lds = (size_t)kShRingBytesPerD * s.head_dim;
+    // two workgroups per CU up to 4 waves (5-slot rings), else one (8 slots)
+    p->attn_stages = p->wr <= 4 ? 5 : 8;
+    p->attn_lds = (size_t)shared_ring_bytes(s.head_dim, p->attn_stages);
     p->attn_wg_target = kCUs * (p->wr <= 4 ? 2 : 1);
   } else {
     p->wr = rg < 4 ? rg : 4;
@@ -213,7 +216,7 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   int32_t* cnt = reinterpret_cast<int32_t*>(ws + plan->off_cnt);
 
   if (!plan->lds_ready.load(std::memory_order_acquire)) {
-    const hipError_t e = plan->attn_shared ? set_tree_attn_shared_lds_limit(s.head_dim, plan->nb, plan->attn_lds)
+    const hipError_t e = plan->attn_shared ? set_tree_attn_shared_lds_limit(s.head_dim, plan->attn_stages, plan->attn_lds)
                                            : set_tree_attn_lds_limit(s.dtype, s.head_dim, plan->nb, plan->attn_lds);
     if (e != hipSuccess) return RESPEC_ERR_HIP;
     plan->lds_ready.store(true, std::memory_order_release);
@@ -252,7 +255,8 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   dim3 agrid(at.nsplit, s.n_kv_heads * plan->n_rowblk, a.batch);
   const hipError_t ae =
       plan->attn_shared
-          ? launch_tree_attn_shared(s.head_dim, plan->nb, agrid, plan->attn_threads, plan->attn_lds, at, st)
+          ? launch_tree_attn_shared(s.head_dim, plan->nb, plan->attn_stages, agrid, plan->attn_threads,
+                                    plan->attn_lds, at, st)
           : launch_tree_attn(s.dtype, s.head_dim, plan->nb, agrid, plan->attn_threads, plan->attn_lds, at, st);
   if (ae != hipSuccess) return RESPEC_ERR_HIP;
   const int merge_rows = 256 / (s.head_dim / 4);

@@ -24,8 +24,6 @@
 //     x = round(h + O) (one workgroup alone cannot pull the partials of a
 //     head fast enough: a single CU's memory parallelism caps it at tens of
 //     GB/s).
-#include <type_traits>
-
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -341,7 +339,7 @@ template <int D, int NB>
 __device__ __forceinline__ void softmax_p_bf16(f32x4 (&s)[2][NB], int t0, int kv_hi, int L, const int (&qnode)[NB],
                                                const u32x4 (&anc)[NB], float scale_log2, float (&m_run)[NB],
                                                float (&l_run)[NB], f32x4 (&o)[D / 16][NB], int lane,
-                                               u32x4 (&phi)[NB], u32x4 (&plo)[NB]) {
+                                               u32x4 (&phi)[NB], u32x4 (&plo)[NB], int nbc = NB) {
   constexpr int DB = D / 16;
   const int lg = lane >> 4;
   typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -364,6 +362,7 @@ __device__ __forceinline__ void softmax_p_bf16(f32x4 (&s)[2][NB], int t0, int kv
   }
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
+    if (nb >= nbc) break;  // row blocks past nbc hold no live row (wave-uniform)
     float tm = kNegInf;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -398,6 +397,7 @@ __device__ __forceinline__ void softmax_p_bf16(f32x4 (&s)[2][NB], int t0, int kv
   // P^T fragments, hi + lo bf16 parts
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
+    if (nb >= nbc) break;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const float p0 = s[j >> 1][nb][2 * (j & 1)], p1 = s[j >> 1][nb][2 * (j & 1) + 1];
@@ -412,11 +412,12 @@ __device__ __forceinline__ void softmax_p_bf16(f32x4 (&s)[2][NB], int t0, int kv
 // O^T += V^T P^T for the output blocks db0 .. db0 + N - 1 (vf[j] holds block db0 + j).
 template <int D, int NB, int N>
 __device__ __forceinline__ void pv_bf16(const u32x4 (&vf)[N], int db0, const u32x4 (&phi)[NB],
-                                        const u32x4 (&plo)[NB], f32x4 (&o)[D / 16][NB]) {
+                                        const u32x4 (&plo)[NB], f32x4 (&o)[D / 16][NB], int nbc = NB) {
 #pragma unroll
-  for (int j = 0; j < N; ++j) {
+  for (int nb = 0; nb < NB; ++nb) {
+    if (nb >= nbc) break;  // row blocks past nbc hold no live row (wave-uniform)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
+    for (int j = 0; j < N; ++j) {
       o[db0 + j][nb] = mma_k64(bf16_t{}, vf[j], phi[nb], o[db0 + j][nb]);
       o[db0 + j][nb] = mma_k64(bf16_t{}, vf[j], plo[nb], o[db0 + j][nb]);
     }
@@ -682,12 +683,15 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
 // Shared-tile variant (bf16; a KV head's query rows span 2-8 waves).  Every
 // wave of such a workgroup needs the same KV rows, so each KV tile is fetched
 // once per workgroup, straight into LDS by DMA (global_load_lds, 16 bytes per
-// lane), into a ring of kShStages slots:
+// lane), into a ring of S slots:
 //   - wave 0 requests the K half and wave 1 the V half of every tile;
-//   - tile i is consumed while tiles i+1 .. i+3 are in flight: a requesting
-//     wave waits until only its two newest tiles are pending, then one barrier
+//   - tile i is consumed while tiles i+1 .. i+S-1 are in flight: a requesting
+//     wave waits until only its S-2 newest tiles are pending, then one barrier
 //     publishes tile i to every wave and, as every wave has finished tile i-1
-//     by then, frees that slot for tile i+3, requested right after;
+//     by then, frees that slot for tile i+S-1, requested right after.  A
+//     loaded HBM request takes several microseconds here, so the ring is
+//     sized to keep most of the CU's LDS in flight (S = 5 with two workgroups
+//     per CU, S = 8 with one);
 //   - K fragments (A operand of S^T = K Q^T) and transposed V fragments are
 //     read from LDS by hand-issued DS instructions that carry their own wait.
 //     The compiler does not see these reads, so it does not make them wait for
@@ -696,8 +700,6 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
 // K slot layout: 32 rows x D bf16, chunk c of row r at chunk position
 // c ^ kswz(r), so that a quarter-wave reading one chunk column of 16 rows hits
 // 64 distinct banks; V slots use the layout of the register path (vswz).
-constexpr int kShStages = 4;
-
 template <int D>
 __device__ __forceinline__ int kswz(int r) {
   return D == 128 ? (r & 15) : ((r >> 1) & 7);
@@ -709,6 +711,18 @@ template <int D, bool V>
 __device__ __forceinline__ void dma_half(unsigned char* slot, const char* base, int t0, int kv_hi, int lane) {
   constexpr int CPR = D * 2 / 16;  // 16-byte chunks per row
   constexpr int RPI = 64 / CPR;    // rows per DMA instruction (1 KB)
+  if (t0 + kKvTile <= kv_hi) {
+    // whole tile in range: a uniform tile base plus a fixed 32-bit offset per lane and instruction
+    const char* tb = base + (size_t)t0 * D * 2;
+#pragma unroll
+    for (int q = 0; q < kKvTile / RPI; ++q) {
+      const int r = q * RPI + lane / CPR, pos = lane % CPR;
+      const uint32_t off = (uint32_t)(r * D * 2 + ((pos ^ (V ? vswz<D>(r) : kswz<D>(r))) << 4));
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(tb + off),
+                                       (__attribute__((address_space(3))) void*)(slot + q * 1024), 16, 0, 0);
+    }
+    return;
+  }
 #pragma unroll
   for (int q = 0; q < kKvTile / RPI; ++q) {
     const int r = q * RPI + lane / CPR, pos = lane % CPR;
@@ -796,7 +810,7 @@ __device__ __forceinline__ void lds_vt_half(uint32_t lds0, int lane, int db0, u3
   for (int j = 0; j < N; ++j) vf[j] = u32x4{h0[j].x, h0[j].y, h1[j].x, h1[j].y};
 }
 
-template <int D, int NB>
+template <int D, int NB, int S>
 __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
   constexpr int KCH = D * 2 / 64;
   constexpr int DB = D / 16;
@@ -804,7 +818,7 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
   constexpr int kTile = kKvTile * D * 2;  // bytes of one K or V half-tile
   constexpr int kStage = 2 * kTile;
   constexpr int kLpt = kTile / 1024;      // DMA instructions per half-tile
-  static_assert((kShStages - 1) * kStage + kTile + 16 * D * 2 < 65536, "DS offsets are 16-bit");
+  static_assert(S >= 3 && (S - 2) * kLpt <= 63, "vmcnt holds at most 63 pending requests");
 
   extern __shared__ __align__(16) unsigned char smem[];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)smem;
@@ -857,10 +871,10 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
     }
   }
 
-  // the first kShStages - 1 tiles (kv_hi >= 1, so every clamped row is a valid cache row)
+  // the first S - 1 tiles (kv_hi >= 1, so every clamped row is a valid cache row)
   if (wave < 2) {
 #pragma unroll
-    for (int st = 0; st < kShStages - 1; ++st) {
+    for (int st = 0; st < S - 1; ++st) {
       if (wave == 0)
         dma_half<D, false>(smem + st * kStage, kbase, tile_row(st), kv_hi, lane);
       else
@@ -879,63 +893,50 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
   }
   u32x4 anc[NB];
   ancestor_bits<NB>(qnode, p_lo, p_hi, n_nodes, anc);
+  // row blocks of this wave that hold a live row (blocks past the group's last row are skipped)
+  const int nbc = __builtin_amdgcn_readfirstlane(min(NB, max(0, (R - row_wave + 15) / 16)));
 
-  auto tile_step = [&](auto stage, int i) {
-    constexpr int S = decltype(stage)::value;
-    constexpr int kSlot = S * kStage;
-    constexpr int kNext = ((S + kShStages - 1) % kShStages) * kStage;  // slot of tile i-1, refilled with i+3
-    if (wave < 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((kShStages - 2) * kLpt) : "memory");
+  int slot = 0;  // ring slot of tile i
+  for (int i = 0; i < n_tiles; ++i) {
+    const int refill = slot == 0 ? S - 1 : slot - 1;  // slot of tile i-1, refilled with tile i+S-1
+    if (wave < 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((S - 2) * kLpt) : "memory");
     __builtin_amdgcn_s_barrier();
     if (wave == 0)
-      dma_half<D, false>(smem + kNext, kbase, tile_row(i + kShStages - 1), kv_hi, lane);
+      dma_half<D, false>(smem + refill * kStage, kbase, tile_row(i + S - 1), kv_hi, lane);
     else if (wave == 1)
-      dma_half<D, true>(smem + kNext + kTile, vbase, tile_row(i + kShStages - 1), kv_hi, lane);
+      dma_half<D, true>(smem + refill * kStage + kTile, vbase, tile_row(i + S - 1), kv_hi, lane);
+    const uint32_t k_at = lds0 + slot * kStage, v_at = k_at + kTile;
     // scores, one 16-row half of the tile at a time (fewer live registers)
     f32x4 s[2][NB];
     {
       u32x4 kf[KCH];
-      lds_k_half<D, kSlot>(lds0, lane, kf);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int kb = 0; kb < 2; ++kb) {
+        if (kb == 0)
+          lds_k_half<D, 0>(k_at, lane, kf);
+        else
+          lds_k_half<D, 16 * D * 2>(k_at, lane, kf);
 #pragma unroll
-        for (int kc = 0; kc < KCH; ++kc) acc = mma_k64(bf16_t{}, kf[kc], qf[nb][kc], acc);
-        s[0][nb] = acc;
-      }
-      lds_k_half<D, kSlot + 16 * D * 2>(lds0, lane, kf);
+        for (int nb = 0; nb < NB; ++nb) {
+          if (nb >= nbc) break;
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kc = 0; kc < KCH; ++kc) acc = mma_k64(bf16_t{}, kf[kc], qf[nb][kc], acc);
-        s[1][nb] = acc;
+          for (int kc = 0; kc < KCH; ++kc) acc = mma_k64(bf16_t{}, kf[kc], qf[nb][kc], acc);
+          s[kb][nb] = acc;
+        }
       }
     }
     u32x4 phi[NB], plo[NB];
     softmax_p_bf16<D, NB>(s, kv_lo + i * kKvTile, kv_hi, L, qnode, anc, a.scale_log2, m_run, l_run, o, lane, phi,
-                          plo);
+                          plo, nbc);
     // O^T += V^T P^T, half of the output blocks at a time
     u32x4 vf[DB / 2];
-    lds_vt_half<D, kSlot + kTile>(lds0, lane, 0, vf);
-    pv_bf16<D, NB, DB / 2>(vf, 0, phi, plo, o);
-    lds_vt_half<D, kSlot + kTile>(lds0, lane, DB / 2, vf);
-    pv_bf16<D, NB, DB / 2>(vf, DB / 2, phi, plo, o);
-  };
-  using S0 = std::integral_constant<int, 0>;
-  using S1 = std::integral_constant<int, 1>;
-  using S2 = std::integral_constant<int, 2>;
-  using S3 = std::integral_constant<int, 3>;
-  static_assert(kShStages == 4, "the loop below walks four slots");
-  int i = 0;
-  for (; i + 3 < n_tiles; i += 4) {
-    tile_step(S0{}, i);
-    tile_step(S1{}, i + 1);
-    tile_step(S2{}, i + 2);
-    tile_step(S3{}, i + 3);
+    lds_vt_half<D, 0>(v_at, lane, 0, vf);
+    pv_bf16<D, NB, DB / 2>(vf, 0, phi, plo, o, nbc);
+    lds_vt_half<D, 0>(v_at, lane, DB / 2, vf);
+    pv_bf16<D, NB, DB / 2>(vf, DB / 2, phi, plo, o, nbc);
+    slot = slot == S - 1 ? 0 : slot + 1;
   }
-  if (i < n_tiles) tile_step(S0{}, i);
-  if (i + 1 < n_tiles) tile_step(S1{}, i + 1);
-  if (i + 2 < n_tiles) tile_step(S2{}, i + 2);
   // the DMAs past the last tile must land before the workgroup's LDS is released
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
@@ -1060,34 +1061,35 @@ hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int thre
 }
 
 template <int D>
-static hipError_t shared_nb(int nb, bool launch, dim3 grid, int threads, size_t lds, const AttnArgs& a,
-                            hipStream_t s) {
+static hipError_t shared_ring(int stages, bool launch, dim3 grid, int threads, size_t lds, const AttnArgs& a,
+                              hipStream_t s) {
   const void* f = nullptr;
-  switch (nb) {
-    case 1: f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 1>); break;
-    case 2: f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2>); break;
+  switch (stages) {
+    case 5: f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, 5>); break;
+    case 8: f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, 8>); break;
     default: return hipErrorInvalidValue;
   }
   if (!launch) return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (nb == 1)
-    hipLaunchKernelGGL((tree_attn_shared_kernel<D, 1>), grid, dim3(threads), lds, s, a);
+  if (stages == 5)
+    hipLaunchKernelGGL((tree_attn_shared_kernel<D, 2, 5>), grid, dim3(threads), lds, s, a);
   else
-    hipLaunchKernelGGL((tree_attn_shared_kernel<D, 2>), grid, dim3(threads), lds, s, a);
+    hipLaunchKernelGGL((tree_attn_shared_kernel<D, 2, 8>), grid, dim3(threads), lds, s, a);
   return hipGetLastError();
 }
 
-hipError_t launch_tree_attn_shared(int head_dim, int nb, dim3 grid, int threads, size_t lds, const AttnArgs& a,
-                                   hipStream_t s) {
-  if (threads < 128 || threads > 512 || threads % 64) return hipErrorInvalidValue;  // 2..8 waves
-  if (head_dim == 128) return shared_nb<128>(nb, true, grid, threads, lds, a, s);
-  if (head_dim == 64) return shared_nb<64>(nb, true, grid, threads, lds, a, s);
+hipError_t launch_tree_attn_shared(int head_dim, int nb, int stages, dim3 grid, int threads, size_t lds,
+                                   const AttnArgs& a, hipStream_t s) {
+  if (nb != 2 || threads < 128 || threads > 512 || threads % 64) return hipErrorInvalidValue;  // 2..8 waves
+  if (lds < (size_t)shared_ring_bytes(head_dim, stages)) return hipErrorInvalidValue;
+  if (head_dim == 128) return shared_ring<128>(stages, true, grid, threads, lds, a, s);
+  if (head_dim == 64) return shared_ring<64>(stages, true, grid, threads, lds, a, s);
   return hipErrorInvalidValue;
 }
 
-hipError_t set_tree_attn_shared_lds_limit(int head_dim, int nb, size_t lds) {
+hipError_t set_tree_attn_shared_lds_limit(int head_dim, int stages, size_t lds) {
   const AttnArgs none{};
-  if (head_dim == 128) return shared_nb<128>(nb, false, dim3(), 0, lds, none, nullptr);
-  if (head_dim == 64) return shared_nb<64>(nb, false, dim3(), 0, lds, none, nullptr);
+  if (head_dim == 128) return shared_ring<128>(stages, false, dim3(), 0, lds, none, nullptr);
+  if (head_dim == 64) return shared_ring<64>(stages, false, dim3(), 0, lds, none, nullptr);
   return hipErrorInvalidValue;
 }
 

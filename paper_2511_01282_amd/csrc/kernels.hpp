@@ -64,11 +64,12 @@ hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int thre
                             const AttnArgs& a, hipStream_t s);
 hipError_t set_tree_attn_lds_limit(int dtype, int head_dim, int nb, size_t lds);
 hipError_t launch_attn_merge(int dtype, int head_dim, dim3 grid, const AttnArgs& a, hipStream_t s);
-// bf16 only; 2-8 waves, each owning 16*nb query rows; KV tiles shared through an LDS ring
-hipError_t launch_tree_attn_shared(int head_dim, int nb, dim3 grid, int threads, size_t lds, const AttnArgs& a,
-                                   hipStream_t s);
-hipError_t set_tree_attn_shared_lds_limit(int head_dim, int nb, size_t lds);
-constexpr int kShRingBytesPerD = 4 * 2 * 32 * 2;  // LDS bytes of the shared-tile ring per unit of head_dim
+// bf16 only; 2-8 waves, each owning 32 query rows (nb = 2); KV tiles shared
+// through an LDS ring of `stages` (5 or 8) K+V tiles
+hipError_t launch_tree_attn_shared(int head_dim, int nb, int stages, dim3 grid, int threads, size_t lds,
+                                   const AttnArgs& a, hipStream_t s);
+hipError_t set_tree_attn_shared_lds_limit(int head_dim, int stages, size_t lds);
+constexpr int shared_ring_bytes(int head_dim, int stages) { return stages * 2 * kKvTile * head_dim * 2; }
 hipError_t launch_lmhead(int dtype, int mb, int ko, const LmArgs& a, hipStream_t s);
 constexpr int kLmTileRows = 64;  // vocabulary rows per LM-head workgroup (one statistics tile)
 hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s);
