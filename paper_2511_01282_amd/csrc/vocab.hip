@@ -13,7 +13,12 @@
 //      handed over with device-coherent stores and loads) runs the look-ahead
 //      procedure on every root-to-leaf chain (64-bit chain masks, one lane per
 //      leaf) and picks the winner: longest accepted length, then smallest last
-//      accepted node, then smallest leaf.
+//      accepted node, then smallest leaf.  Every row checks the sequence's tree
+//      and walks its leaf chains before taking the ticket (that needs only the
+//      parents), so the winner of the ticket only reads the predicates.
+// A row is reduced by four waves (one when the vocabulary has at most 64
+// tiles): each wave reduces its lanes' partials by wave-wide reductions and a
+// top-K by repeated maxima, then wave 0 combines the waves.
 // Extra workgroups (one per sequence) report sequences whose node range is
 // unusable, since no row workgroup would finish them.
 #include "common.hpp"
@@ -37,15 +42,77 @@ __device__ __forceinline__ uint64_t wave_min_u64(uint64_t x) {
   return x;
 }
 
-// Look-ahead tolerance on one chain u_1..u_d; bit s-1 of G / OK describes u_s.
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
+  uint64_t y;
+  y = xchg<0>(x); x = y > x ? y : x;
+  y = xchg<1>(x); x = y > x ? y : x;
+  y = xchg<2>(x); x = y > x ? y : x;
+  y = xchg<3>(x); x = y > x ? y : x;
+  y = xchg<4>(x); x = y > x ? y : x;
+  y = xchg<5>(x); x = y > x ? y : x;
+  return x;
+}
+
+// Top K keys of a wave whose lanes each hold a descending list of L keys:
+// K rounds of "wave maximum of the lanes' heads, whose owner pops it".  Keys
+// are distinct (the low word holds the token id) or 0 (empty slot).  Every
+// lane receives the same top[].
+template <int L, int K>
+__device__ __forceinline__ void wave_topk(uint64_t (&key)[L], uint64_t (&top)[K]) {
+#pragma unroll
+  for (int r = 0; r < K; ++r) {
+    const uint64_t mx = wave_max_u64(key[0]);
+    top[r] = mx;
+    const bool pop = key[0] == mx;
+#pragma unroll
+    for (int k = 0; k + 1 < L; ++k) key[k] = pop ? key[k + 1] : key[k];
+    key[L - 1] = pop ? 0ull : key[L - 1];
+  }
+}
+
+// Softmax statistics of the wave's union of disjoint sets: the maximum first,
+// then every lane's sums rescaled to it (T = sum e^(z-M) (z-M)) and added; the
+// argmax is the smallest id among lanes at the maximum.
+__device__ __forceinline__ void wave_rowstats(RowStats& st) {
+  float M = st.m;
+  M = fmaxf(M, xchg<0>(M));
+  M = fmaxf(M, xchg<1>(M));
+  M = fmaxf(M, xchg<2>(M));
+  M = fmaxf(M, xchg<3>(M));
+  M = fmaxf(M, xchg<4>(M));
+  M = fmaxf(M, xchg<5>(M));
+  const bool empty = st.m == -__builtin_huge_valf();
+  const float d = empty ? 0.f : st.m - M;
+  const float e = empty ? 0.f : __expf(d);
+  float S = st.S * e, T = (st.T + d * st.S) * e;
+  int am = (!empty && st.m == M) ? st.am : 0x7FFFFFFF;
+  S += xchg<0>(S); T += xchg<0>(T); am = min(am, xchg<0>(am));
+  S += xchg<1>(S); T += xchg<1>(T); am = min(am, xchg<1>(am));
+  S += xchg<2>(S); T += xchg<2>(T); am = min(am, xchg<2>(am));
+  S += xchg<3>(S); T += xchg<3>(T); am = min(am, xchg<3>(am));
+  S += xchg<4>(S); T += xchg<4>(T); am = min(am, xchg<4>(am));
+  S += xchg<5>(S); T += xchg<5>(T); am = min(am, xchg<5>(am));
+  st.m = M;
+  st.S = S;
+  st.T = T;
+  st.am = am;
+}
+
+// Look-ahead tolerance on one chain u_1..u_d; bit s-1 of G / OK describes u_s
+// (no bits at or above d).  Runs of greedy matches are counted with
+// count-trailing-zeros of the complement.
+__device__ __forceinline__ int ones_from(uint64_t G, int s) {  // consecutive set bits of G from bit s up
+  if (s >= 64) return 0;
+  const uint64_t z = ~(G >> s);
+  return z == 0 ? 64 - s : __builtin_ctzll(z);
+}
+
 __device__ __forceinline__ int lookahead_bits(int d, uint64_t G, uint64_t OK, int m, int phi) {
-  int l0 = 0;
-  while (l0 < d && ((G >> l0) & 1ull)) ++l0;
+  const int l0 = ones_from(G, 0);
   int cur = l0, last = l0;
   for (int att = 0; att < phi && cur < d; ++att) {
     if (!((OK >> cur) & 1ull)) break;
-    int xi = 0;
-    while (cur + 1 + xi < d && ((G >> (cur + 1 + xi)) & 1ull)) ++xi;
+    const int xi = ones_from(G, cur + 1);
     if (xi >= m) {
       last = cur + 1 + xi;
       cur = last;
@@ -120,19 +187,22 @@ __device__ void write_seq_error(const VocabArgs& a, int b, int status, int n0, i
   }
 }
 
-// One wave: validate sequence b and reduce its accepted path.  The sequence's
-// parents, tokens and tags are already in LDS; its predicate bits and argmaxes
-// (written by the other row workgroups) are read once with device-coherent
-// loads.  Every lane walks its leaves' chains once (recording the chain in
-// LDS), so no chain step touches global memory.
-__device__ void path_reduce(const VocabArgs& a, int b, int n0, int n, int L, const int* s_par, const int* s_tok,
-                            const uint8_t* s_src, uint8_t* s_flag, uint8_t* s_hc, int* s_am, uint8_t* s_chain,
-                            int lane) {
+// Chains of the leaves of one sequence, walked once per row workgroup before
+// the completion ticket (they need only the parents, which every row holds in
+// LDS).  Lane l owns leaves l and l + 64; chain[it][l][k] is the node k steps
+// above leaf l + 64*it (the leaf itself at k = 0), depth[it] its depth, or -1
+// for a node with children.
+struct PathPrep {
+  int depth[2];
+  bool bad_tree, bad_tok, too_deep;
+};
+
+__device__ __forceinline__ PathPrep path_prepare(const VocabArgs& a, int n, const int* s_par, const int* s_tok,
+                                                 const uint8_t* s_src, uint8_t* s_hc, uint8_t* s_chain, int lane) {
+  PathPrep pp{{-1, -1}, false, false, false};
   bool bad_tree = false, bad_tok = false;
   for (int j = lane; j < n; j += 64) {
     const int p = s_par[j];
-    s_flag[j] = (uint8_t)ld_dev(a.flag_ws + n0 + j);
-    s_am[j] = ld_dev(a.argmax + n0 + j);
     s_hc[j] = 0;
     if (j == 0) {
       bad_tree |= p != -1;
@@ -142,52 +212,81 @@ __device__ void path_reduce(const VocabArgs& a, int b, int n0, int n, int L, con
       bad_tok |= t < 0 || t >= a.vocab || s_src[j] > 1;
     }
   }
-  bad_tree = __any(bad_tree);
-  bad_tok = __any(bad_tok);
-  const bool bad_cap = L < 0 || L > a.max_kv || L > a.kv_cap - n;
-  uint64_t best = ~0ull;
-  if (!bad_tree) {
-    wave_lds_sync();
-    for (int j = lane; j < n; j += 64)
-      if (j > 0) s_hc[s_par[j]] = 1;
-    wave_lds_sync();
-    // parents strictly decrease, so every walk ends at the root within n steps
-    uint8_t* chain = s_chain + lane * kMaxDepth;
-    bool too_deep = false;
-    for (int j = lane; j < n; j += 64) {
-      if (s_hc[j]) {
-        a.leaf_acc_len[n0 + j] = -1;
-        continue;
-      }
-      uint64_t g_rev = 0, ok_rev = 0;  // bit k describes the node k steps above the leaf
-      int d = 0, x = j;
-      while (x != 0 && d < kMaxDepth) {
-        chain[d] = (uint8_t)x;
-        const uint32_t f = s_flag[x];
-        g_rev |= (uint64_t)(f & kFlagGreedy) << d;
-        ok_rev |= (uint64_t)((f & (kFlagGreedy | kFlagRelaxed)) != 0) << d;
-        x = s_par[x];
-        ++d;
-      }
-      if (x != 0 || d > a.max_depth) {
-        too_deep = true;
-        continue;
-      }
-      // bit s-1 of G / OK describes u_s, the node at depth s
-      const uint64_t G = d ? (__builtin_bitreverse64(g_rev) >> (64 - d)) : 0ull;
-      const uint64_t OK = d ? (__builtin_bitreverse64(ok_rev) >> (64 - d)) : 0ull;
-      const int acc = lookahead_bits(d, G, OK, a.min_lookahead, a.max_relaxed);
-      const int e = acc == 0 ? 0 : chain[d - acc];
-      a.leaf_acc_len[n0 + j] = acc;
-      const uint64_t key = ((uint64_t)(kMaxDepth - acc) << 40) | ((uint64_t)e << 20) | (uint64_t)j;
-      best = key < best ? key : best;
+  pp.bad_tree = __any(bad_tree);
+  pp.bad_tok = __any(bad_tok);
+  if (pp.bad_tree) return pp;
+  wave_lds_sync();
+  for (int j = lane; j < n; j += 64)
+    if (j > 0) s_hc[s_par[j]] = 1;
+  wave_lds_sync();
+  // parents strictly decrease, so every walk ends at the root within n steps
+  bool too_deep = false;
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const int j = lane + 64 * it;
+    if (j >= n || s_hc[j]) continue;
+    uint8_t* chain = s_chain + (it * 64 + lane) * kMaxDepth;
+    int d = 0, x = j;
+    while (x != 0 && d < kMaxDepth) {
+      chain[d] = (uint8_t)x;
+      x = s_par[x];
+      ++d;
     }
-    bad_tree = __any(too_deep);
+    if (x != 0 || d > a.max_depth) {
+      too_deep = true;
+      continue;
+    }
+    pp.depth[it] = d;
   }
-  const int status = bad_tree ? kStatusTree : bad_tok ? kStatusToken : bad_cap ? kStatusCapacity : 0;
+  pp.too_deep = __any(too_deep);
+  return pp;
+}
+
+// One wave, after winning the sequence's ticket: read every node's predicate
+// bits and argmax (written by the other rows), run the look-ahead procedure on
+// the chains prepared above, and write the winner, its path and the flags.
+__device__ void path_finish(const VocabArgs& a, int b, int n0, int n, int L, const PathPrep& pp, const int* s_par,
+                            uint8_t* s_flag, int* s_am, const uint8_t* s_chain, int lane) {
+  const bool bad_cap = L < 0 || L > a.max_kv || L > a.kv_cap - n;
+  const bool bad_tree = pp.bad_tree || pp.too_deep;
+  const int status = bad_tree ? kStatusTree : pp.bad_tok ? kStatusToken : bad_cap ? kStatusCapacity : 0;
   if (status != 0) {
     write_seq_error(a, b, status, n0, n, lane);
     return;
+  }
+  for (int j = lane; j < n; j += 64) {
+    s_flag[j] = (uint8_t)ld_dev(a.flag_ws + n0 + j);
+    s_am[j] = ld_dev(a.argmax + n0 + j);
+  }
+  wave_lds_sync();
+  uint64_t best = ~0ull;
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const int j = lane + 64 * it;
+    if (j >= n) continue;
+    const int d = pp.depth[it];
+    if (d < 0) {
+      a.leaf_acc_len[n0 + j] = -1;
+      continue;
+    }
+    const uint8_t* chain = s_chain + (it * 64 + lane) * kMaxDepth;
+    uint64_t G = 0, OK = 0;  // bit s-1 describes u_s, the node at depth s (chain[d - s])
+    for (int k0 = 0; k0 < d; k0 += 8) {
+      const uint64_t c8 = *reinterpret_cast<const uint64_t*>(chain + k0);  // 8 chain entries at once
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int k = k0 + u;
+        const uint32_t f = k < d ? s_flag[(c8 >> (8 * u)) & 0xFFu] : 0u;
+        const int bit = d - 1 - k;
+        G |= k < d ? (uint64_t)(f & kFlagGreedy) << bit : 0ull;
+        OK |= k < d ? (uint64_t)((f & (kFlagGreedy | kFlagRelaxed)) != 0) << bit : 0ull;
+      }
+    }
+    const int acc = lookahead_bits(d, G, OK, a.min_lookahead, a.max_relaxed);
+    const int e = acc == 0 ? 0 : chain[d - acc];
+    a.leaf_acc_len[n0 + j] = acc;
+    const uint64_t key = ((uint64_t)(kMaxDepth - acc) << 40) | ((uint64_t)e << 20) | (uint64_t)j;
+    best = key < best ? key : best;
   }
   best = wave_min_u64(best);
   const int acc = kMaxDepth - (int)(best >> 40);
@@ -224,23 +323,25 @@ struct FinalizeLds {
   int node_am[kMaxNodes];
   uint8_t flag[kMaxNodes];
   uint8_t hc[kMaxNodes];
-  uint8_t chain[64 * kMaxDepth];
+  alignas(8) uint8_t chain[2 * 64 * kMaxDepth];
   int ticket;
 };
 
 // One node row: statistics, children's predicates, and (last row of the
-// sequence) the path.  Wide: batch >= 64 (node offsets in several groups).
-template <int KO, bool Wide>
+// sequence) the path.  WPR waves reduce the row (1 or 4).  Wide: batch >= 64
+// (node offsets in several groups).
+template <int KO, int WPR, bool Wide>
 __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>& sh) {
   constexpr int W = TilePartial<KO>::kWords;
-  constexpr int kLoadBatch = 2;  // tile partials per thread requested up front
+  constexpr int kLoadBatch = WPR == 1 ? 1 : 8;  // tile partials per thread requested up front
+  constexpr int NT = 64 * WPR;   // threads of the row
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int tid = threadIdx.x;
   const int i = blockIdx.x;
 
   // Requests, in the order their data is needed later: the node offsets, this
-  // thread's tile partials, then (once the sequence is known) one node's
-  // parent, token and tag per thread.  All are issued by every lane with
+  // thread's tile partials, then (once the sequence is known) the parent, token
+  // and tag of nodes tid and tid + NT.  All are issued by every lane with
   // clamped indices, so the load counts are the same on every path.
   const uint32_t* prow = reinterpret_cast<const uint32_t*>(a.partials) + (size_t)i * a.n_vtiles * W;
   u32x4 buf[kLoadBatch][W / 4];
@@ -248,7 +349,7 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
   load_offsets(a, lane, v0, vn0);
 #pragma unroll
   for (int u = 0; u < kLoadBatch; ++u) {
-    const int t = min(tid + u * (int)blockDim.x, a.n_vtiles - 1);
+    const int t = min(tid + u * NT, a.n_vtiles - 1);
 #pragma unroll
     for (int q = 0; q < W / 4; ++q) buf[u][q] = *reinterpret_cast<const u32x4*>(prow + (size_t)t * W + 4 * q);
   }
@@ -256,97 +357,117 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
   const bool lay_ok = lay.ok;
   const int b = lay.b, n0 = lay.n0, n = lay.n;
   const int li = i - n0;
-  const int jn = lay_ok ? n0 + min(tid, n - 1) : 0;
-  const int c_par = a.parent[jn];
-  const int c_tok = a.token[jn];
-  const int c_src = a.src[jn];
+  constexpr int NPT = (kMaxNodes + NT - 1) / NT;  // nodes described per thread
+  int c_par[NPT], c_tok[NPT], c_src[NPT];
+#pragma unroll
+  for (int u = 0; u < NPT; ++u) {
+    const int jn = lay_ok ? n0 + min(tid + u * NT, n - 1) : 0;
+    c_par[u] = a.parent[jn];
+    c_tok[u] = a.token[jn];
+    c_src[u] = a.src[jn];
+  }
+  const int kv_b = a.kv_len[lay_ok ? b : 0];
 
-  // fold the row's tile partials: this thread's tiles, then the wave
+  // fold the row's tile partials: this thread's tiles (the first is taken as it is)
   RowStats st;
   st.init();
   uint64_t key[KO];
 #pragma unroll
   for (int k = 0; k < KO; ++k) key[k] = 0ull;
-  auto fold = [&](const u32x4 (&pb)[W / 4]) {
-    st.merge(__uint_as_float(pb[0][0]), __uint_as_float(pb[0][1]), __uint_as_float(pb[0][2]), (int)pb[0][3]);
-    uint64_t pk[KO];
+  auto unpack = [&](const u32x4 (&pb)[W / 4], uint64_t (&pk)[KO]) {
 #pragma unroll
     for (int k = 0; k < KO; ++k) {
       const u32x4 w4 = pb[1 + k / 2];
       pk[k] = (k & 1) ? (((uint64_t)w4[3] << 32) | w4[2]) : (((uint64_t)w4[1] << 32) | w4[0]);
     }
+  };
+  auto fold = [&](const u32x4 (&pb)[W / 4]) {
+    st.merge(__uint_as_float(pb[0][0]), __uint_as_float(pb[0][1]), __uint_as_float(pb[0][2]), (int)pb[0][3]);
+    uint64_t pk[KO];
+    unpack(pb, pk);
     merge_topk<KO>(key, pk);
   };
+  if (tid < a.n_vtiles) {
+    st.m = __uint_as_float(buf[0][0][0]);
+    st.S = __uint_as_float(buf[0][0][1]);
+    st.T = __uint_as_float(buf[0][0][2]);
+    st.am = (int)buf[0][0][3];
+    unpack(buf[0], key);
+  }
 #pragma unroll
-  for (int u = 0; u < kLoadBatch; ++u)
-    if (tid + u * (int)blockDim.x < a.n_vtiles) fold(buf[u]);
-  for (int t = tid + kLoadBatch * blockDim.x; t < a.n_vtiles; t += blockDim.x) {
+  for (int u = 1; u < kLoadBatch; ++u)
+    if (tid + u * NT < a.n_vtiles) fold(buf[u]);
+  for (int t = tid + kLoadBatch * NT; t < a.n_vtiles; t += NT) {
     u32x4 pb[W / 4];
 #pragma unroll
     for (int q = 0; q < W / 4; ++q) pb[q] = *reinterpret_cast<const u32x4*>(prow + (size_t)t * W + 4 * q);
     fold(pb);
   }
-  st.merge_level<0>();
-  merge_topk_level<KO, 0>(key);
-  st.merge_level<1>();
-  merge_topk_level<KO, 1>(key);
-  st.merge_level<2>();
-  merge_topk_level<KO, 2>(key);
-  // the children of node li request their logit z_li[t] while the merge goes on
-  // (scheduling barriers keep the request here, after the parents have had time to arrive)
-  __builtin_amdgcn_sched_barrier(0);
-  const bool is_child = lay_ok && tid < n && tid > 0 && c_par == li;
-  const bool tok_ok = c_tok >= 0 && c_tok < a.vocab;
-  const float c_z = a.logits[(size_t)i * a.vocab + (is_child && tok_ok ? c_tok : 0)];
-  __builtin_amdgcn_sched_barrier(0);
-  st.merge_level<3>();
-  merge_topk_level<KO, 3>(key);
-  st.merge_level<4>();
-  merge_topk_level<KO, 4>(key);
-  st.merge_level<5>();
-  merge_topk_level<KO, 5>(key);
-  if (lane == 0) {
-    sh.st[wave][0] = st.m;
-    sh.st[wave][1] = st.S;
-    sh.st[wave][2] = st.T;
-    sh.st[wave][3] = __int_as_float(st.am);
+  // the children of node li request their logit z_li[t] now (the parents have had time to arrive)
+  bool is_child[NPT], tok_ok[NPT];
+  float c_z[NPT];
 #pragma unroll
-    for (int k = 0; k < KO; ++k) sh.key[wave][k] = key[k];
+  for (int u = 0; u < NPT; ++u) {
+    const int j = tid + u * NT;
+    is_child[u] = lay_ok && j < n && j > 0 && c_par[u] == li;
+    tok_ok[u] = c_tok[u] >= 0 && c_tok[u] < a.vocab;
+    c_z[u] = a.logits[(size_t)i * a.vocab + (is_child[u] && tok_ok[u] ? c_tok[u] : 0)];
   }
-  if (lay_ok && tid < n) {
-    sh.par[tid] = c_par;
-    sh.tok[tid] = c_tok;
-    sh.src[tid] = (uint8_t)c_src;
-  }
-  __syncthreads();
-  // across the 4 waves (wave 0; lanes of a quad hold the 4 wave results); the
-  // row's results go to LDS first and to memory after the barrier, so that the
-  // barrier does not wait for the stores
-  if (wave == 0) {
-    const int src_wave = lane & 3;
-    st.m = sh.st[src_wave][0];
-    st.S = sh.st[src_wave][1];
-    st.T = sh.st[src_wave][2];
-    st.am = __float_as_int(sh.st[src_wave][3]);
+  // the wave: statistics by reductions, top-K by repeated maxima
+  wave_rowstats(st);
+  uint64_t top[KO];
+  wave_topk<KO, KO>(key, top);
+  // the sequence's nodes go to LDS (the path reduction reads them)
+  if (lay_ok) {
 #pragma unroll
-    for (int k = 0; k < KO; ++k) key[k] = sh.key[src_wave][k];
-    st.merge_level<0>();
-    merge_topk_level<KO, 0>(key);
-    st.merge_level<1>();
-    merge_topk_level<KO, 1>(key);
-    if (lane == 0) {
-      sh.row[0] = st.m;
-      sh.row[1] = st.m + __logf(st.S);
-      sh.row[3] = __int_as_float(st.am);
-#pragma unroll
-      for (int k = 0; k < KO; ++k) sh.top[k] = key[k];
+    for (int u = 0; u < NPT; ++u) {
+      const int j = tid + u * NT;
+      if (j < n) {
+        sh.par[j] = c_par[u];
+        sh.tok[j] = c_tok[u];
+        sh.src[j] = (uint8_t)c_src[u];
+      }
     }
   }
-  __syncthreads();
+  if constexpr (WPR > 1) {
+    if (lane == 0) {
+      sh.st[wave][0] = st.m;
+      sh.st[wave][1] = st.S;
+      sh.st[wave][2] = st.T;
+      sh.st[wave][3] = __int_as_float(st.am);
+    }
+    if (lane < KO) {
+      uint64_t mine = top[0];
+#pragma unroll
+      for (int k = 1; k < KO; ++k) mine = lane == k ? top[k] : mine;
+      sh.key[wave][lane] = mine;
+    }
+    __syncthreads();
+    // across the waves (wave 0): lane w < WPR brings wave w's statistics, lane
+    // l < WPR*KO one key of wave l / KO's list
+    if (wave == 0) {
+      const bool src_ok = lane < WPR;
+      st.m = src_ok ? sh.st[lane][0] : -__builtin_huge_valf();
+      st.S = src_ok ? sh.st[lane][1] : 0.f;
+      st.T = src_ok ? sh.st[lane][2] : 0.f;
+      st.am = src_ok ? __float_as_int(sh.st[lane][3]) : 0x7FFFFFFF;
+      wave_rowstats(st);
+      uint64_t k1[1] = {lane < WPR * KO ? sh.key[lane / KO][lane % KO] : 0ull};
+      wave_topk<1, KO>(k1, top);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < KO; ++k) key[k] = top[k];
+  // row results: LDS for the predicates, memory for the outputs (wave 0)
   if (wave == 0) {
     const float logS = __logf(st.S);
     const float lse = st.m + logS;
     if (lane == 0) {
+      sh.row[0] = st.m;
+      sh.row[1] = lse;
+      sh.row[3] = __int_as_float(st.am);
+#pragma unroll
+      for (int k = 0; k < KO; ++k) sh.top[k] = key[k];
       a.max_logit[i] = st.m;
       st_dev(a.argmax + i, st.am);
       a.lse[i] = lse;
@@ -359,44 +480,58 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
         a.topk_logprob[(size_t)i * a.topk_out + k] = key_value(key[k]) - lse;
       }
   }
+  if constexpr (WPR > 1)
+    __syncthreads();
+  else
+    wave_lds_sync();
   if (!lay_ok) return;  // uniform over the workgroup
 
-  // predicates of the children of node li: thread j describes node j
-  if (is_child) {
+  // predicates of the children of node li: thread j describes node j (and j + NT)
+#pragma unroll
+  for (int u = 0; u < NPT; ++u) {
+    if (!is_child[u]) continue;
+    const int j = tid + u * NT;
     const float m = sh.row[0], lse = sh.row[1];
     const int am = __float_as_int(sh.row[3]);
     uint32_t f = 0;
     float lp = 0.f;
-    if (tok_ok) {
+    if (tok_ok[u]) {
       bool intop = false;
 #pragma unroll
-      for (int k = 0; k < KO; ++k) intop |= (k < a.topk) && (key_id(sh.top[k]) == c_tok);
-      if (c_tok == am) f |= kFlagGreedy;
+      for (int k = 0; k < KO; ++k) intop |= (k < a.topk) && (key_id(sh.top[k]) == c_tok[u]);
+      if (c_tok[u] == am) f |= kFlagGreedy;
       if (intop) f |= kFlagTopk;
-      if ((double)m - (double)c_z <= (double)a.tau) f |= kFlagTau;
-      if (c_src == 1 && (f & kFlagTopk) && (f & kFlagTau)) f |= kFlagRelaxed;
-      lp = c_z - lse;
+      if ((double)m - (double)c_z[u] <= (double)a.tau) f |= kFlagTau;
+      if (c_src[u] == 1 && (f & kFlagTopk) && (f & kFlagTau)) f |= kFlagRelaxed;
+      lp = c_z[u] - lse;
     }
-    st_dev(a.flag_ws + n0 + tid, (int32_t)f);
-    a.tok_logprob[n0 + tid] = lp;
+    st_dev(a.flag_ws + n0 + j, (int32_t)f);
+    a.tok_logprob[n0 + j] = lp;
   }
   if (li == 0 && tid == 0) {
     st_dev(a.flag_ws + n0, 0);
     a.tok_logprob[n0] = 0.f;
   }
 
+  // tree checks and leaf chains (wave 0) while the stores drain
+  PathPrep pp{};
+  if (wave == 0) pp = path_prepare(a, n, sh.par, sh.tok, sh.src, sh.hc, sh.chain, lane);
+
   // ---- sequence completion ticket ----
   stores_done();
-  __syncthreads();
+  if constexpr (WPR > 1) __syncthreads();
   if (tid == 0) sh.ticket = atomicAdd(a.seq_counter + b, 1);
-  __syncthreads();
+  if constexpr (WPR > 1)
+    __syncthreads();
+  else
+    wave_lds_sync();
   if (sh.ticket != n - 1 || wave != 0) return;
-  path_reduce(a, b, n0, n, a.kv_len[b], sh.par, sh.tok, sh.src, sh.flag, sh.hc, sh.node_am, sh.chain, lane);
+  path_finish(a, b, n0, n, kv_b, pp, sh.par, sh.flag, sh.node_am, sh.chain, lane);
   if (lane == 0) st_dev(a.seq_counter + b, 0);
 }
 
-template <int KO>
-__global__ __launch_bounds__(256) void finalize_kernel(VocabArgs a) {
+template <int KO, int WPR>
+__global__ __launch_bounds__(64 * WPR) void finalize_kernel(VocabArgs a) {
   __shared__ FinalizeLds<KO> sh;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (blockIdx.x >= (unsigned)a.total_nodes) {
@@ -411,16 +546,22 @@ __global__ __launch_bounds__(256) void finalize_kernel(VocabArgs a) {
     return;
   }
   if (a.batch < 64)
-    finalize_row<KO, false>(a, sh);
+    finalize_row<KO, WPR, false>(a, sh);
   else
-    finalize_row<KO, true>(a, sh);
+    finalize_row<KO, WPR, true>(a, sh);
 }
 
 hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s) {
-  if (ko == 8)
-    hipLaunchKernelGGL((finalize_kernel<8>), dim3(blocks), dim3(256), 0, s, a);
+  // one wave per row up to 64 vocabulary tiles, else four
+  const bool one = a.n_vtiles <= 64;
+  if (ko == 8 && one)
+    hipLaunchKernelGGL((finalize_kernel<8, 1>), dim3(blocks), dim3(64), 0, s, a);
+  else if (ko == 8)
+    hipLaunchKernelGGL((finalize_kernel<8, 4>), dim3(blocks), dim3(256), 0, s, a);
+  else if (ko == 16 && one)
+    hipLaunchKernelGGL((finalize_kernel<16, 1>), dim3(blocks), dim3(64), 0, s, a);
   else if (ko == 16)
-    hipLaunchKernelGGL((finalize_kernel<16>), dim3(blocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((finalize_kernel<16, 4>), dim3(blocks), dim3(256), 0, s, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
