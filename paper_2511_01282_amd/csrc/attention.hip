@@ -688,14 +688,13 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
 //   - tile i is consumed while tiles i+1 .. i+S-1 are in flight: a requesting
 //     wave waits until only its S-2 newest tiles are pending, then one barrier
 //     publishes tile i to every wave and, as every wave has finished tile i-1
-//     by then, frees that slot for tile i+S-1, requested right after.  A
-//     loaded HBM request takes several microseconds here, so the ring is
-//     sized to keep most of the CU's LDS in flight (S = 5 with two workgroups
-//     per CU, S = 8 with one);
-//   - K fragments (A operand of S^T = K Q^T) and transposed V fragments are
-//     read from LDS by hand-issued DS instructions that carry their own wait.
-//     The compiler does not see these reads, so it does not make them wait for
-//     every DMA in flight (it cannot tell the ring slots apart);
+//     by then, frees that slot for tile i+S-1, requested right after (S = 5
+//     with two workgroups per CU, S = 8 with one); with S-1 tiles in flight
+//     the loop waits on its own arithmetic, not on HBM;
+//   - the DMA requests are inline assembly (see dma_half_asm), so the K
+//     fragments (A operand of S^T = K Q^T) and the transposed V fragments are
+//     ordinary LDS reads that the compiler schedules; the barrier's own waits
+//     order them against the ring;
 //   - each wave owns 16*NB query rows of its own: no cross-wave merge.
 // K slot layout: 32 rows x D bf16, chunk c of row r at chunk position
 // c ^ kswz(r), so that a quarter-wave reading one chunk column of 16 rows hits
@@ -705,109 +704,38 @@ __device__ __forceinline__ int kswz(int r) {
   return D == 128 ? (r & 15) : ((r >> 1) & 7);
 }
 
-// Request one half (K or V) of a 32-row tile into an LDS slot; rows at or past
-// kv_hi are clamped to kv_hi - 1 (masked, or weighted by zero, as above).
+// Request one half (K or V) of a 32-row tile into an LDS slot, 16 bytes per
+// lane (global_load_lds_dwordx4); rows at or past kv_hi are clamped to
+// kv_hi - 1 (masked, or weighted by zero, as above).  Issued as inline
+// assembly so that the compiler does not see an LDS write in flight: it then
+// schedules the ring's LDS reads freely (instead of waiting for every
+// outstanding request before each of them), and the kernel's own waits order
+// them.  The tile base is uniform (scalar registers), each lane adds a 32-bit
+// offset; M0 holds the LDS destination (saved and restored around the
+// request) and needs one wait state before the request.
 template <int D, bool V>
-__device__ __forceinline__ void dma_half(unsigned char* slot, const char* base, int t0, int kv_hi, int lane) {
+__device__ __forceinline__ void dma_half_asm(uint32_t lds_dst, const char* base, int t0, int kv_hi, int lane) {
   constexpr int CPR = D * 2 / 16;  // 16-byte chunks per row
   constexpr int RPI = 64 / CPR;    // rows per DMA instruction (1 KB)
-  if (t0 + kKvTile <= kv_hi) {
-    // whole tile in range: a uniform tile base plus a fixed 32-bit offset per lane and instruction
-    const char* tb = base + (size_t)t0 * D * 2;
-#pragma unroll
-    for (int q = 0; q < kKvTile / RPI; ++q) {
-      const int r = q * RPI + lane / CPR, pos = lane % CPR;
-      const uint32_t off = (uint32_t)(r * D * 2 + ((pos ^ (V ? vswz<D>(r) : kswz<D>(r))) << 4));
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(tb + off),
-                                       (__attribute__((address_space(3))) void*)(slot + q * 1024), 16, 0, 0);
-    }
-    return;
-  }
+  const char* tb = base + (size_t)t0 * D * 2;
+  const bool full = t0 + kKvTile <= kv_hi;  // uniform
 #pragma unroll
   for (int q = 0; q < kKvTile / RPI; ++q) {
     const int r = q * RPI + lane / CPR, pos = lane % CPR;
-    const int p = min(t0 + r, kv_hi - 1);
     const int c = pos ^ (V ? vswz<D>(r) : kswz<D>(r));  // chunk that belongs at position pos
-    __builtin_amdgcn_global_load_lds(
-        (const __attribute__((address_space(1))) void*)(base + (size_t)p * D * 2 + c * 16),
-        (__attribute__((address_space(3))) void*)(slot + q * 1024), 16, 0, 0);
-  }
-}
-
-// K fragments of rows 16*kb .. 16*kb+15 of the slot at LDS byte offset OFF
-// (OFF includes kb): kf[kc] = K[row 16*kb + lr][bytes 64*kc + 16*lg .. +15].
-template <int D, int OFF>
-__device__ __forceinline__ void lds_k_half(uint32_t lds0, int lane, u32x4 (&kf)[D * 2 / 64]) {
-  constexpr int KCH = D * 2 / 64;
-  const int lr = lane & 15, lg = lane >> 4;
-  const int sw = kswz<D>(lr);  // kswz(16 + lr) == kswz(lr)
-  uint32_t ad[KCH];
-#pragma unroll
-  for (int kc = 0; kc < KCH; ++kc) ad[kc] = lds0 + lr * D * 2 + (((4 * kc + lg) ^ sw) << 4);
-  if constexpr (D == 128) {
+    const int rr = full ? r : min(t0 + r, kv_hi - 1) - t0;  // rows past kv_hi: row kv_hi - 1 (t0 <= kv_hi - 1)
+    const uint32_t off = (uint32_t)(rr * D * 2 + c * 16);
+    uint32_t saved;
     asm volatile(
-        "ds_read_b128 %0, %4 offset:%8\n\t"
-        "ds_read_b128 %1, %5 offset:%8\n\t"
-        "ds_read_b128 %2, %6 offset:%8\n\t"
-        "ds_read_b128 %3, %7 offset:%8\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(kf[0]), "=&v"(kf[1]), "=&v"(kf[2]), "=&v"(kf[3])
-        : "v"(ad[0]), "v"(ad[1]), "v"(ad[2]), "v"(ad[3]), "n"(OFF)
-        : "memory");
-  } else {
-    asm volatile(
-        "ds_read_b128 %0, %2 offset:%4\n\t"
-        "ds_read_b128 %1, %3 offset:%4\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(kf[0]), "=&v"(kf[1])
-        : "v"(ad[0]), "v"(ad[1]), "n"(OFF)
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %2, %3\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds_dst + q * 1024), "v"(off), "s"(tb)
         : "memory");
   }
-}
-
-// Transposed V fragments of output blocks db0 .. db0 + D/32 - 1 of the slot at
-// LDS byte offset OFF, as read_vt_bf16 (vf[j] holds block db0 + j).
-template <int D, int OFF>
-__device__ __forceinline__ void lds_vt_half(uint32_t lds0, int lane, int db0, u32x4 (&vf)[D / 32]) {
-  constexpr int N = D / 32;
-  const int lr = lane & 15, lg = lane >> 4;
-  const int r = 4 * lg + lr / 4;
-  const int sw = vswz<D>(r);
-  uint32_t ad[N];
-#pragma unroll
-  for (int j = 0; j < N; ++j) {
-    const int col = 16 * (db0 + j) + 4 * (lr % 4);
-    ad[j] = lds0 + r * (D * 2) + (((col >> 3) ^ sw) << 4) + (col & 7) * 2;
-  }
-  u32x2 h0[N], h1[N];
-  if constexpr (D == 128) {
-    asm volatile(
-        "ds_read_b64_tr_b16 %0, %8 offset:%12\n\t"
-        "ds_read_b64_tr_b16 %4, %8 offset:%13\n\t"
-        "ds_read_b64_tr_b16 %1, %9 offset:%12\n\t"
-        "ds_read_b64_tr_b16 %5, %9 offset:%13\n\t"
-        "ds_read_b64_tr_b16 %2, %10 offset:%12\n\t"
-        "ds_read_b64_tr_b16 %6, %10 offset:%13\n\t"
-        "ds_read_b64_tr_b16 %3, %11 offset:%12\n\t"
-        "ds_read_b64_tr_b16 %7, %11 offset:%13\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(h0[0]), "=&v"(h0[1]), "=&v"(h0[2]), "=&v"(h0[3]), "=&v"(h1[0]), "=&v"(h1[1]), "=&v"(h1[2]),
-          "=&v"(h1[3])
-        : "v"(ad[0]), "v"(ad[1]), "v"(ad[2]), "v"(ad[3]), "n"(OFF), "n"(OFF + 16 * D * 2)
-        : "memory");
-  } else {
-    asm volatile(
-        "ds_read_b64_tr_b16 %0, %4 offset:%6\n\t"
-        "ds_read_b64_tr_b16 %2, %4 offset:%7\n\t"
-        "ds_read_b64_tr_b16 %1, %5 offset:%6\n\t"
-        "ds_read_b64_tr_b16 %3, %5 offset:%7\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(h0[0]), "=&v"(h0[1]), "=&v"(h1[0]), "=&v"(h1[1])
-        : "v"(ad[0]), "v"(ad[1]), "n"(OFF), "n"(OFF + 16 * D * 2)
-        : "memory");
-  }
-#pragma unroll
-  for (int j = 0; j < N; ++j) vf[j] = u32x4{h0[j].x, h0[j].y, h1[j].x, h1[j].y};
 }
 
 template <int D, int NB, int S>
@@ -876,9 +804,9 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
 #pragma unroll
     for (int st = 0; st < S - 1; ++st) {
       if (wave == 0)
-        dma_half<D, false>(smem + st * kStage, kbase, tile_row(st), kv_hi, lane);
+        dma_half_asm<D, false>(lds0 + st * kStage, kbase, tile_row(st), kv_hi, lane);
       else
-        dma_half<D, true>(smem + st * kStage + kTile, vbase, tile_row(st), kv_hi, lane);
+        dma_half_asm<D, true>(lds0 + st * kStage + kTile, vbase, tile_row(st), kv_hi, lane);
     }
   }
 
@@ -899,42 +827,43 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
   int slot = 0;  // ring slot of tile i
   for (int i = 0; i < n_tiles; ++i) {
     const int refill = slot == 0 ? S - 1 : slot - 1;  // slot of tile i-1, refilled with tile i+S-1
-    if (wave < 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((S - 2) * kLpt) : "memory");
-    __builtin_amdgcn_s_barrier();
+    // tile i has landed (a requesting wave waits for its own requests) and every
+    // wave's reads of tile i-1 are done: one barrier covers both
+    if (wave < 2)
+      asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"((S - 2) * kLpt) : "memory");
+    else
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     if (wave == 0)
-      dma_half<D, false>(smem + refill * kStage, kbase, tile_row(i + S - 1), kv_hi, lane);
+      dma_half_asm<D, false>(lds0 + refill * kStage, kbase, tile_row(i + S - 1), kv_hi, lane);
     else if (wave == 1)
-      dma_half<D, true>(smem + refill * kStage + kTile, vbase, tile_row(i + S - 1), kv_hi, lane);
-    const uint32_t k_at = lds0 + slot * kStage, v_at = k_at + kTile;
-    // scores, one 16-row half of the tile at a time (fewer live registers)
-    f32x4 s[2][NB];
+      dma_half_asm<D, true>(lds0 + refill * kStage + kTile, vbase, tile_row(i + S - 1), kv_hi, lane);
+    const unsigned char* kt = smem + slot * kStage;
+    KTile<D> kf;
     {
-      u32x4 kf[KCH];
+      const int sw = kswz<D>(lr);  // kswz(16 + lr) == kswz(lr)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        if (kb == 0)
-          lds_k_half<D, 0>(k_at, lane, kf);
-        else
-          lds_k_half<D, 16 * D * 2>(k_at, lane, kf);
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          if (nb >= nbc) break;
-          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int kc = 0; kc < KCH; ++kc) acc = mma_k64(bf16_t{}, kf[kc], qf[nb][kc], acc);
-          s[kb][nb] = acc;
-        }
-      }
+        for (int kc = 0; kc < KCH; ++kc)
+          kf.k[kb][kc] = *reinterpret_cast<const u32x4*>(kt + (16 * kb + lr) * D * 2 + (((4 * kc + lg) ^ sw) << 4));
     }
+    f32x4 s[2][NB];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        if (nb >= nbc) break;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < KCH; ++kc) acc = mma_k64(bf16_t{}, kf.k[kb][kc], qf[nb][kc], acc);
+        s[kb][nb] = acc;
+      }
+    u32x4 vf[DB];
+    read_vt_bf16<D>(kt + kTile, lane, vf);
     u32x4 phi[NB], plo[NB];
     softmax_p_bf16<D, NB>(s, kv_lo + i * kKvTile, kv_hi, L, qnode, anc, a.scale_log2, m_run, l_run, o, lane, phi,
                           plo, nbc);
-    // O^T += V^T P^T, half of the output blocks at a time
-    u32x4 vf[DB / 2];
-    lds_vt_half<D, 0>(v_at, lane, 0, vf);
-    pv_bf16<D, NB, DB / 2>(vf, 0, phi, plo, o, nbc);
-    lds_vt_half<D, 0>(v_at, lane, DB / 2, vf);
-    pv_bf16<D, NB, DB / 2>(vf, DB / 2, phi, plo, o, nbc);
+    pv_bf16<D, NB, DB>(vf, 0, phi, plo, o, nbc);
     slot = slot == S - 1 ? 0 : slot + 1;
   }
   // the DMAs past the last tile must land before the workgroup's LDS is released
