@@ -157,8 +157,9 @@ def main():
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / K
 
-    # per-stage durations: a second pass of K steps with HIP events recorded by the
-    # library on the step's stream before and after each stage
+    # per-stage durations: a second pass of K steps with HIP events that the library
+    # takes from the kernels' own dispatches (start of attention, end of the split
+    # merge, of the LM head and of the vocabulary pass), on the step's stream
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
     for row in evs:
         for e in row:

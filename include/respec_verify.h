@@ -146,9 +146,11 @@ typedef struct {
   int32_t* winner_leaf;     /* [B] sequence-local leaf whose chain won, -1 on error         */
   int32_t* seq_status;      /* [B] RESPEC_OK, RESPEC_ERR_TREE or RESPEC_ERR_TOKEN           */
 
-  void* stage_events;       /* optional host array of 4 hipEvent_t recorded on the stream
-                               before attention, before the LM head, before the vocab pass
-                               and after the step (profiling); NULL = none                  */
+  void* stage_events;       /* optional host array of 4 hipEvent_t (profiling), NULL = none:
+                               [0] start of the attention kernel, [1] end of the split
+                               merge, [2] end of the LM head, [3] end of the vocab pass,
+                               each taken from that kernel's own dispatch (a stage that
+                               does not run records its event on the stream instead)      */
 } respec_verify_args;
 
 typedef struct respec_verify_plan respec_verify_plan;

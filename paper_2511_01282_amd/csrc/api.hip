@@ -221,7 +221,6 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
     if (e != hipSuccess) return RESPEC_ERR_HIP;
     plan->lds_ready.store(true, std::memory_order_release);
   }
-  if (ev && hipEventRecord(ev[0], st) != hipSuccess) return RESPEC_ERR_HIP;
 
   // ---- tree-masked attention + residual ----
   AttnArgs at;
@@ -256,13 +255,14 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   const hipError_t ae =
       plan->attn_shared
           ? launch_tree_attn_shared(s.head_dim, plan->nb, plan->attn_stages, agrid, plan->attn_threads,
-                                    plan->attn_lds, at, st)
-          : launch_tree_attn(s.dtype, s.head_dim, plan->nb, agrid, plan->attn_threads, plan->attn_lds, at, st);
+                                    plan->attn_lds, at, st, ev ? ev[0] : nullptr)
+          : launch_tree_attn(s.dtype, s.head_dim, plan->nb, agrid, plan->attn_threads, plan->attn_lds, at, st,
+                             ev ? ev[0] : nullptr);
   if (ae != hipSuccess) return RESPEC_ERR_HIP;
   const int merge_rows = 256 / (s.head_dim / 4);
   dim3 mgrid(cdiv(plan->rows_per_wg, merge_rows), a.batch * s.n_kv_heads * plan->n_rowblk);
-  if (launch_attn_merge(s.dtype, s.head_dim, mgrid, at, st) != hipSuccess) return RESPEC_ERR_HIP;
-  if (ev && hipEventRecord(ev[1], st) != hipSuccess) return RESPEC_ERR_HIP;
+  if (launch_attn_merge(s.dtype, s.head_dim, mgrid, at, st, ev ? ev[1] : nullptr) != hipSuccess)
+    return RESPEC_ERR_HIP;
 
   // ---- LM head ----
   if (need_logits) {
@@ -281,9 +281,10 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
     lm.n_mtiles = cdiv(M, 16 * mb);
     lm.partials = full ? reinterpret_cast<float*>(ws + plan->off_part) : nullptr;
     lm.n_vtiles = plan->n_vtiles;
-    if (launch_lmhead(s.dtype, mb, plan->ko, lm, st) != hipSuccess) return RESPEC_ERR_HIP;
+    if (launch_lmhead(s.dtype, mb, plan->ko, lm, st, ev ? ev[2] : nullptr) != hipSuccess) return RESPEC_ERR_HIP;
+  } else if (ev && hipEventRecord(ev[2], st) != hipSuccess) {
+    return RESPEC_ERR_HIP;
   }
-  if (ev && hipEventRecord(ev[2], st) != hipSuccess) return RESPEC_ERR_HIP;
 
   // ---- row statistics, predicates, path ----
   if (full) {
@@ -324,9 +325,11 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
     v.min_lookahead = a.accept.min_lookahead;
     v.max_relaxed = a.accept.max_relaxed;
     v.tau = a.accept.tau;
-    if (launch_finalize(plan->ko, a.total_nodes + a.batch, v, st) != hipSuccess) return RESPEC_ERR_HIP;
+    if (launch_finalize(plan->ko, a.total_nodes + a.batch, v, st, ev ? ev[3] : nullptr) != hipSuccess)
+      return RESPEC_ERR_HIP;
+  } else if (ev && hipEventRecord(ev[3], st) != hipSuccess) {
+    return RESPEC_ERR_HIP;
   }
-  if (ev && hipEventRecord(ev[3], st) != hipSuccess) return RESPEC_ERR_HIP;
   return RESPEC_OK;
 }
 

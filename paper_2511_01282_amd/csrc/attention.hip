@@ -960,13 +960,13 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 }
 
 template <typename T, int D>
-static hipError_t launch_nb(int nb, dim3 grid, int threads, size_t lds, const AttnArgs& a, hipStream_t s) {
+static hipError_t launch_nb(int nb, dim3 grid, int threads, size_t lds, const AttnArgs& a, hipStream_t s,
+                            hipEvent_t ev_start) {
   switch (nb) {
-    case 1: hipLaunchKernelGGL((tree_attn_kernel<T, D, 1>), grid, dim3(threads), lds, s, a); break;
-    case 2: hipLaunchKernelGGL((tree_attn_kernel<T, D, 2>), grid, dim3(threads), lds, s, a); break;
+    case 1: return launch_k(tree_attn_kernel<T, D, 1>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
+    case 2: return launch_k(tree_attn_kernel<T, D, 2>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 template <typename T, int D>
@@ -981,17 +981,17 @@ static hipError_t set_lds_nb(int nb, size_t lds) {
 }
 
 hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int threads, size_t lds,
-                            const AttnArgs& a, hipStream_t s) {
-  if (dtype == 1 && head_dim == 128) return launch_nb<bf16_t, 128>(nb, grid, threads, lds, a, s);
-  if (dtype == 1 && head_dim == 64) return launch_nb<bf16_t, 64>(nb, grid, threads, lds, a, s);
-  if (dtype == 0 && head_dim == 128) return launch_nb<float, 128>(nb, grid, threads, lds, a, s);
-  if (dtype == 0 && head_dim == 64) return launch_nb<float, 64>(nb, grid, threads, lds, a, s);
+                            const AttnArgs& a, hipStream_t s, hipEvent_t ev_start) {
+  if (dtype == 1 && head_dim == 128) return launch_nb<bf16_t, 128>(nb, grid, threads, lds, a, s, ev_start);
+  if (dtype == 1 && head_dim == 64) return launch_nb<bf16_t, 64>(nb, grid, threads, lds, a, s, ev_start);
+  if (dtype == 0 && head_dim == 128) return launch_nb<float, 128>(nb, grid, threads, lds, a, s, ev_start);
+  if (dtype == 0 && head_dim == 64) return launch_nb<float, 64>(nb, grid, threads, lds, a, s, ev_start);
   return hipErrorInvalidValue;
 }
 
 template <int D>
 static hipError_t shared_ring(int stages, bool launch, dim3 grid, int threads, size_t lds, const AttnArgs& a,
-                              hipStream_t s) {
+                              hipStream_t s, hipEvent_t ev_start) {
   const void* f = nullptr;
   switch (stages) {
     case 5: f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, 5>); break;
@@ -999,41 +999,34 @@ static hipError_t shared_ring(int stages, bool launch, dim3 grid, int threads, s
     default: return hipErrorInvalidValue;
   }
   if (!launch) return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (stages == 5)
-    hipLaunchKernelGGL((tree_attn_shared_kernel<D, 2, 5>), grid, dim3(threads), lds, s, a);
-  else
-    hipLaunchKernelGGL((tree_attn_shared_kernel<D, 2, 8>), grid, dim3(threads), lds, s, a);
-  return hipGetLastError();
+  if (stages == 5) return launch_k(tree_attn_shared_kernel<D, 2, 5>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
+  return launch_k(tree_attn_shared_kernel<D, 2, 8>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
 }
 
 hipError_t launch_tree_attn_shared(int head_dim, int nb, int stages, dim3 grid, int threads, size_t lds,
-                                   const AttnArgs& a, hipStream_t s) {
+                                   const AttnArgs& a, hipStream_t s, hipEvent_t ev_start) {
   if (nb != 2 || threads < 128 || threads > 512 || threads % 64) return hipErrorInvalidValue;  // 2..8 waves
   if (lds < (size_t)shared_ring_bytes(head_dim, stages)) return hipErrorInvalidValue;
-  if (head_dim == 128) return shared_ring<128>(stages, true, grid, threads, lds, a, s);
-  if (head_dim == 64) return shared_ring<64>(stages, true, grid, threads, lds, a, s);
+  if (head_dim == 128) return shared_ring<128>(stages, true, grid, threads, lds, a, s, ev_start);
+  if (head_dim == 64) return shared_ring<64>(stages, true, grid, threads, lds, a, s, ev_start);
   return hipErrorInvalidValue;
 }
 
 hipError_t set_tree_attn_shared_lds_limit(int head_dim, int stages, size_t lds) {
   const AttnArgs none{};
-  if (head_dim == 128) return shared_ring<128>(stages, false, dim3(), 0, lds, none, nullptr);
-  if (head_dim == 64) return shared_ring<64>(stages, false, dim3(), 0, lds, none, nullptr);
+  if (head_dim == 128) return shared_ring<128>(stages, false, dim3(), 0, lds, none, nullptr, nullptr);
+  if (head_dim == 64) return shared_ring<64>(stages, false, dim3(), 0, lds, none, nullptr, nullptr);
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_attn_merge(int dtype, int head_dim, dim3 grid, const AttnArgs& a, hipStream_t s) {
-  if (dtype == 1 && head_dim == 128)
-    hipLaunchKernelGGL((attn_merge_kernel<bf16_t, 128>), grid, dim3(256), 0, s, a);
-  else if (dtype == 1 && head_dim == 64)
-    hipLaunchKernelGGL((attn_merge_kernel<bf16_t, 64>), grid, dim3(256), 0, s, a);
-  else if (dtype == 0 && head_dim == 128)
-    hipLaunchKernelGGL((attn_merge_kernel<float, 128>), grid, dim3(256), 0, s, a);
-  else if (dtype == 0 && head_dim == 64)
-    hipLaunchKernelGGL((attn_merge_kernel<float, 64>), grid, dim3(256), 0, s, a);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+hipError_t launch_attn_merge(int dtype, int head_dim, dim3 grid, const AttnArgs& a, hipStream_t s,
+                             hipEvent_t ev_stop) {
+  const dim3 blk(256);
+  if (dtype == 1 && head_dim == 128) return launch_k(attn_merge_kernel<bf16_t, 128>, grid, blk, 0, s, nullptr, ev_stop, a);
+  if (dtype == 1 && head_dim == 64) return launch_k(attn_merge_kernel<bf16_t, 64>, grid, blk, 0, s, nullptr, ev_stop, a);
+  if (dtype == 0 && head_dim == 128) return launch_k(attn_merge_kernel<float, 128>, grid, blk, 0, s, nullptr, ev_stop, a);
+  if (dtype == 0 && head_dim == 64) return launch_k(attn_merge_kernel<float, 64>, grid, blk, 0, s, nullptr, ev_stop, a);
+  return hipErrorInvalidValue;
 }
 
 hipError_t set_tree_attn_lds_limit(int dtype, int head_dim, int nb, size_t lds) {

@@ -1,6 +1,7 @@
 // Internal launch interface of the verification kernels (not part of the C ABI).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -59,20 +60,35 @@ struct VocabArgs {
   float tau;
 };
 
-// dtype-dispatching launchers (0 = f32, 1 = bf16); return hipSuccess or the launch error
+// Launch a kernel whose single argument is an argument struct.  Optional
+// start / stop events take the dispatch's own timestamps (hipExtLaunchKernel),
+// so a stage timed with them matches the kernel's duration.
+template <typename F, typename A>
+inline hipError_t launch_k(F kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, hipEvent_t ev_start,
+                           hipEvent_t ev_stop, const A& args) {
+  if (ev_start || ev_stop)
+    hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, s, ev_start, ev_stop, 0u, args);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, lds, s, args);
+  return hipGetLastError();
+}
+
+// dtype-dispatching launchers (0 = f32, 1 = bf16); return hipSuccess or the launch error.
+// ev_start / ev_stop: optional timing events (see launch_k).
 hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int threads, size_t lds,
-                            const AttnArgs& a, hipStream_t s);
+                            const AttnArgs& a, hipStream_t s, hipEvent_t ev_start = nullptr);
 hipError_t set_tree_attn_lds_limit(int dtype, int head_dim, int nb, size_t lds);
-hipError_t launch_attn_merge(int dtype, int head_dim, dim3 grid, const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn_merge(int dtype, int head_dim, dim3 grid, const AttnArgs& a, hipStream_t s,
+                             hipEvent_t ev_stop = nullptr);
 // bf16 only; 2-8 waves, each owning 32 query rows (nb = 2); KV tiles shared
 // through an LDS ring of `stages` (5 or 8) K+V tiles
 hipError_t launch_tree_attn_shared(int head_dim, int nb, int stages, dim3 grid, int threads, size_t lds,
-                                   const AttnArgs& a, hipStream_t s);
+                                   const AttnArgs& a, hipStream_t s, hipEvent_t ev_start = nullptr);
 hipError_t set_tree_attn_shared_lds_limit(int head_dim, int stages, size_t lds);
 constexpr int shared_ring_bytes(int head_dim, int stages) { return stages * 2 * kKvTile * head_dim * 2; }
-hipError_t launch_lmhead(int dtype, int mb, int ko, const LmArgs& a, hipStream_t s);
+hipError_t launch_lmhead(int dtype, int mb, int ko, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
 constexpr int kLmTileRows = 64;  // vocabulary rows per LM-head workgroup (one statistics tile)
-hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s);
+hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
 hipError_t launch_zero_i32(int32_t* p, size_t n, hipStream_t s);
 
 }  // namespace respec

@@ -463,18 +463,18 @@ __global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
 }
 
 template <typename T, int KO>
-static hipError_t launch_mb(int mb, dim3 grid, const LmArgs& a, hipStream_t s) {
+static hipError_t launch_mb(int mb, dim3 grid, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop) {
+  const dim3 blk(256);
   switch (mb) {
-    case 1: hipLaunchKernelGGL((lmhead_kernel<T, 1, KO>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((lmhead_kernel<T, 2, KO>), grid, dim3(256), 0, s, a); break;
-    case 3: hipLaunchKernelGGL((lmhead_kernel<T, 3, KO>), grid, dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((lmhead_kernel<T, 4, KO>), grid, dim3(256), 0, s, a); break;
+    case 1: return launch_k(lmhead_kernel<T, 1, KO>, grid, blk, 0, s, nullptr, ev_stop, a);
+    case 2: return launch_k(lmhead_kernel<T, 2, KO>, grid, blk, 0, s, nullptr, ev_stop, a);
+    case 3: return launch_k(lmhead_kernel<T, 3, KO>, grid, blk, 0, s, nullptr, ev_stop, a);
+    case 4: return launch_k(lmhead_kernel<T, 4, KO>, grid, blk, 0, s, nullptr, ev_stop, a);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
-hipError_t launch_lmhead(int dtype, int mb, int ko, const LmArgs& a, hipStream_t s) {
+hipError_t launch_lmhead(int dtype, int mb, int ko, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop) {
   const int n_vt = (a.vocab + kLmRows - 1) / kLmRows;
   const int n_grp = (n_vt + 7) / 8;
   dim3 grid(n_grp * 8 * a.n_mtiles);
@@ -482,20 +482,20 @@ hipError_t launch_lmhead(int dtype, int mb, int ko, const LmArgs& a, hipStream_t
     if (dtype != 1) return hipErrorInvalidValue;
     const int n_vt2 = (a.vocab + kTlRows - 1) / kTlRows;
     dim3 tgrid(((n_vt2 + 7) / 8) * 8 * a.n_mtiles);
+    const dim3 blk(256);
     const int tmb = mb / 2;
-    if (ko == 8) {
-      if (tmb == 4) hipLaunchKernelGGL((lmhead_tiled_kernel<4, 8>), tgrid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((lmhead_tiled_kernel<8, 8>), tgrid, dim3(256), 0, s, a);
-    } else if (ko == 16) {
-      if (tmb == 4) hipLaunchKernelGGL((lmhead_tiled_kernel<4, 16>), tgrid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((lmhead_tiled_kernel<8, 16>), tgrid, dim3(256), 0, s, a);
-    } else {
-      return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
+    if (ko == 8)
+      return tmb == 4 ? launch_k(lmhead_tiled_kernel<4, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a)
+                      : launch_k(lmhead_tiled_kernel<8, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a);
+    if (ko == 16)
+      return tmb == 4 ? launch_k(lmhead_tiled_kernel<4, 16>, tgrid, blk, 0, s, nullptr, ev_stop, a)
+                      : launch_k(lmhead_tiled_kernel<8, 16>, tgrid, blk, 0, s, nullptr, ev_stop, a);
+    return hipErrorInvalidValue;
   }
-  if (ko == 8) return dtype == 1 ? launch_mb<bf16_t, 8>(mb, grid, a, s) : launch_mb<float, 8>(mb, grid, a, s);
-  if (ko == 16) return dtype == 1 ? launch_mb<bf16_t, 16>(mb, grid, a, s) : launch_mb<float, 16>(mb, grid, a, s);
+  if (ko == 8)
+    return dtype == 1 ? launch_mb<bf16_t, 8>(mb, grid, a, s, ev_stop) : launch_mb<float, 8>(mb, grid, a, s, ev_stop);
+  if (ko == 16)
+    return dtype == 1 ? launch_mb<bf16_t, 16>(mb, grid, a, s, ev_stop) : launch_mb<float, 16>(mb, grid, a, s, ev_stop);
   return hipErrorInvalidValue;
 }
 

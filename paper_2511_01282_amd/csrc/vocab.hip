@@ -551,20 +551,14 @@ __global__ __launch_bounds__(64 * WPR) void finalize_kernel(VocabArgs a) {
     finalize_row<KO, WPR, true>(a, sh);
 }
 
-hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s) {
+hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s, hipEvent_t ev_stop) {
   // one wave per row up to 64 vocabulary tiles, else four
   const bool one = a.n_vtiles <= 64;
-  if (ko == 8 && one)
-    hipLaunchKernelGGL((finalize_kernel<8, 1>), dim3(blocks), dim3(64), 0, s, a);
-  else if (ko == 8)
-    hipLaunchKernelGGL((finalize_kernel<8, 4>), dim3(blocks), dim3(256), 0, s, a);
-  else if (ko == 16 && one)
-    hipLaunchKernelGGL((finalize_kernel<16, 1>), dim3(blocks), dim3(64), 0, s, a);
-  else if (ko == 16)
-    hipLaunchKernelGGL((finalize_kernel<16, 4>), dim3(blocks), dim3(256), 0, s, a);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+  if (ko == 8 && one) return launch_k(finalize_kernel<8, 1>, dim3(blocks), dim3(64), 0, s, nullptr, ev_stop, a);
+  if (ko == 8) return launch_k(finalize_kernel<8, 4>, dim3(blocks), dim3(256), 0, s, nullptr, ev_stop, a);
+  if (ko == 16 && one) return launch_k(finalize_kernel<16, 1>, dim3(blocks), dim3(64), 0, s, nullptr, ev_stop, a);
+  if (ko == 16) return launch_k(finalize_kernel<16, 4>, dim3(blocks), dim3(256), 0, s, nullptr, ev_stop, a);
+  return hipErrorInvalidValue;
 }
 
 __global__ void zero_i32_kernel(int32_t* p, size_t n) {
