@@ -8,12 +8,12 @@
 // Tiling: a workgroup owns 64 vocabulary rows (4 waves x 16) and one tile of
 // 16*MB token rows; about two workgroups share a CU.  The contraction runs on
 // the matrix cores with W as the A operand and x as the B operand.
-//   - W fragments (16 bytes per lane) go straight from HBM to registers in a
-//     two-deep pipeline: while K step c is multiplied, step c+1 is in flight
-//     and step c+2 is issued right after.
+//   - W fragments (16 bytes per lane) go straight from HBM to registers, and
+//     each thread's share of the x tile with them, in a ring of two or three K
+//     steps: while step c is multiplied the next ones are in flight, and the
+//     requests of step c + ring are issued right after (memory counters drain
+//     in issue order, so waiting for step c never waits for newer requests).
 //   - x is staged per 512-byte K step in a double-buffered, padded LDS tile.
-//     Its loads are issued before the next W loads, so waiting for them never
-//     waits for W (memory counters drain in issue order).
 //   - Tiles are numbered so that the M tiles of one vocabulary tile run on the
 //     same XCD at the same time and share W through that XCD's L2.
 // Output lane layout gives each lane 4 consecutive vocabulary entries of one
@@ -31,43 +31,12 @@ constexpr int kLmChunkBytes = 512;                  // bytes of a row per K step
 constexpr int kLmPieces = kLmChunkBytes / 64;       // mma_k64 calls per K step
 constexpr int kLmXStride = kLmChunkBytes + 16;      // LDS row stride of the x tile
 
+// x tile of one K step: 16*MB token rows x 512 bytes, in 16-byte pieces
 template <int MB>
 struct XStage {
   static constexpr int kPieces = 16 * MB * (kLmChunkBytes / 16);  // 16-byte pieces per tile
   static constexpr int kPerThread = (kPieces + 255) / 256;
-  u32x4 v[kPerThread];
 };
-
-template <int MB>
-__device__ __forceinline__ void x_load(XStage<MB>& xs, const char* xbase, size_t row_bytes, int m0, int m_rows,
-                                       int step) {
-#pragma unroll
-  for (int t = 0; t < XStage<MB>::kPerThread; ++t) {
-    const int idx = threadIdx.x + 256 * t;
-    const int r = idx / (kLmChunkBytes / 16), pc = idx % (kLmChunkBytes / 16);
-    const int m = m0 + r;
-    xs.v[t] = (idx < XStage<MB>::kPieces && m < m_rows)
-                  ? ld16(xbase + (size_t)m * row_bytes + (size_t)step * kLmChunkBytes + pc * 16)
-                  : u32x4{0, 0, 0, 0};
-  }
-}
-
-template <int MB>
-__device__ __forceinline__ void x_store(const XStage<MB>& xs, unsigned char* sx) {
-#pragma unroll
-  for (int t = 0; t < XStage<MB>::kPerThread; ++t) {
-    const int idx = threadIdx.x + 256 * t;
-    if (idx < XStage<MB>::kPieces) {
-      const int r = idx / (kLmChunkBytes / 16), pc = idx % (kLmChunkBytes / 16);
-      *reinterpret_cast<u32x4*>(sx + r * kLmXStride + pc * 16) = xs.v[t];
-    }
-  }
-}
-
-__device__ __forceinline__ void w_load(u32x4 (&w)[kLmPieces], const char* wrow, bool ok, size_t off) {
-#pragma unroll
-  for (int kp = 0; kp < kLmPieces; ++kp) w[kp] = ok ? ld16(wrow + off + kp * 64) : u32x4{0, 0, 0, 0};
-}
 
 template <typename T, int MB>
 __device__ __forceinline__ void mma_step(f32x4 (&acc)[MB], const u32x4 (&w)[kLmPieces], const unsigned char* sx,
@@ -196,40 +165,96 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmArgs a) {
   // ranges of their rows, which spreads the requests over the memory channels
   // (rows are 8 KB apart, so equal column offsets would land on the same ones).
   const int rot = vt % n_steps;
-  const int v = vw + lr;
-  const bool wok = v < a.vocab;
-  const char* wrow = reinterpret_cast<const char*>(a.w) + (size_t)(wok ? v : 0) * row_bytes + lg * 16;
+  auto step_of = [&](int c) { return c + rot < n_steps ? c + rot : c + rot - n_steps; };
+  const int v = min(vw + lr, a.vocab - 1);  // rows past V: a valid row, results not stored
+  const char* wrow = reinterpret_cast<const char*>(a.w) + (size_t)v * row_bytes + lg * 16;
   const char* xbase = reinterpret_cast<const char*>(a.x);
 
   f32x4 acc[MB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  u32x4 wa[kLmPieces], wb[kLmPieces];
-  XStage<MB> xs;
-  auto step_of = [&](int c) { return c + rot < n_steps ? c + rot : c + rot - n_steps; };
-  w_load(wa, wrow, wok, (size_t)step_of(0) * kLmChunkBytes);
-  if (n_steps > 1) w_load(wb, wrow, wok, (size_t)step_of(1) * kLmChunkBytes);
-  x_load<MB>(xs, xbase, row_bytes, m0, a.m_rows, step_of(0));
-  x_store<MB>(xs, sx[0]);
-  __syncthreads();
-
-  for (int c = 0; c < n_steps; c += 2) {
-    // ---- step c: wa, sx[0] ----
-    if (c + 1 < n_steps) x_load<MB>(xs, xbase, row_bytes, m0, a.m_rows, step_of(c + 1));
-    mma_step<T, MB>(acc, wa, sx[0], lr, lg);
-    if (c + 2 < n_steps) w_load(wa, wrow, wok, (size_t)step_of(c + 2) * kLmChunkBytes);
-    if (c + 1 >= n_steps) break;
-    x_store<MB>(xs, sx[1]);
-    __syncthreads();
-    // ---- step c+1: wb, sx[1] ----
-    if (c + 2 < n_steps) x_load<MB>(xs, xbase, row_bytes, m0, a.m_rows, step_of(c + 2));
-    mma_step<T, MB>(acc, wb, sx[1], lr, lg);
-    if (c + 3 < n_steps) w_load(wb, wrow, wok, (size_t)step_of(c + 3) * kLmChunkBytes);
-    if (c + 2 < n_steps) {
-      x_store<MB>(xs, sx[0]);
-      __syncthreads();
+  // A ring of kStages K steps in registers: the W fragments and this thread's
+  // share of the x tile of step c + kStages are requested together, right after
+  // step c's products, so waiting for step c never waits for newer requests.
+  // (Rows shorter than the ring: the slots past the last step are requested
+  // with clamped steps and never consumed.)
+  constexpr int kStages = MB == 3 ? 3 : 2;
+  constexpr int XPT = XStage<MB>::kPerThread;
+  static_assert(XStage<MB>::kPieces % 256 == 0, "every thread stages whole pieces of x");
+  struct Stage {
+    u32x4 w[kLmPieces];
+    u32x4 x[XPT];
+  };
+  auto issue = [&](Stage& st, int c) {
+    const size_t off = (size_t)step_of(c) * kLmChunkBytes;
+#pragma unroll
+    for (int kp = 0; kp < kLmPieces; ++kp) st.w[kp] = ld16(wrow + off + kp * 64);
+#pragma unroll
+    for (int t = 0; t < XPT; ++t) {
+      const int idx = threadIdx.x + 256 * t;
+      const int r = idx / (kLmChunkBytes / 16), pc = idx % (kLmChunkBytes / 16);
+      const int m = min(m0 + r, a.m_rows - 1);  // rows past M: a valid row, results not stored
+      st.x[t] = ld16(xbase + (size_t)m * row_bytes + off + pc * 16);
     }
+  };
+  auto stage_x = [&](const Stage& st, unsigned char* buf) {
+#pragma unroll
+    for (int t = 0; t < XPT; ++t) {
+      const int idx = threadIdx.x + 256 * t;
+      const int r = idx / (kLmChunkBytes / 16), pc = idx % (kLmChunkBytes / 16);
+      *reinterpret_cast<u32x4*>(buf + r * kLmXStride + pc * 16) = st.x[t];
+    }
+  };
+  // x alternates between two LDS buffers: the barrier of step c+1 orders step
+  // c's reads before the writes of step c+2
+  auto step = [&](Stage& st, int c, bool refill) {
+    unsigned char* buf = sx[c & 1];
+    stage_x(st, buf);
+    __syncthreads();
+    mma_step<T, MB>(acc, st.w, buf, lr, lg);
+    if (refill) issue(st, c + kStages);
+    __builtin_amdgcn_sched_barrier(0);  // keep the requests here, ahead of the next step's wait
+  };
+  auto step_clamped = [&](Stage& st, int c) {
+    unsigned char* buf = sx[c & 1];
+    stage_x(st, buf);
+    __syncthreads();
+    mma_step<T, MB>(acc, st.w, buf, lr, lg);
+    issue(st, min(c + kStages, n_steps - 1));
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  Stage ring[kStages];
+#pragma unroll
+  for (int j = 0; j < kStages; ++j) {
+    issue(ring[j], min(j, n_steps - 1));
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  int c = 0;
+  if constexpr (MB <= 2) {
+    // Steady state: every step refills its slot with a real step, so the count
+    // of requests behind every step is the same on every pass.  The last steps
+    // (at most 2*kStages - 1, straight-line code) refill only while steps
+    // remain: no request is left in flight at the end, where the epilogue's
+    // barriers would wait for it (all workgroups of a small M run at once, so
+    // that wait is not hidden behind other workgroups).
+    for (; c + 2 * kStages <= n_steps; c += kStages) {
+#pragma unroll
+      for (int j = 0; j < kStages; ++j) step(ring[j], c + j, true);
+    }
+#pragma unroll
+    for (int j = 0; j < 2 * kStages - 1; ++j)
+      if (c + j < n_steps) step(ring[j % kStages], c + j, c + j + kStages < n_steps);
+  } else {
+    // (larger x tiles: past the last step the refills repeat the last step, unused,
+    // which keeps the loop's register assignment stable)
+    for (; c + kStages - 1 < n_steps; c += kStages) {
+#pragma unroll
+      for (int j = 0; j < kStages; ++j) step_clamped(ring[j], c + j);
+    }
+#pragma unroll
+    for (int j = 0; j + 1 < kStages; ++j)
+      if (c + j < n_steps) step_clamped(ring[j], c + j);
   }
 
   // lane holds z[m0 + 16*mb + lr][vw + 4*lg + i]
