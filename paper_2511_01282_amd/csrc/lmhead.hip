@@ -378,35 +378,35 @@ __global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
   };
 
   // three stages in a ring: step c is consumed while steps c+1 and c+2 are in
-  // flight; after its products step c+3 goes into the freed registers (past
-  // the end: step n_steps-1 again, unused).  x alternates between two LDS
-  // buffers (the barrier of step c+1 orders step c's reads before the writes
-  // of step c+2).
-  Stage s0, s1, s2;
-  issue(s0, 0);
-  __builtin_amdgcn_sched_barrier(0);
-  issue(s1, 1);
-  __builtin_amdgcn_sched_barrier(0);
-  issue(s2, 2);
-  __builtin_amdgcn_sched_barrier(0);
-  auto step = [&](Stage& st, int c) {
+  // flight; after its products step c+3 goes into the freed registers.  The
+  // steady-state loop only refills real steps (the same count of requests
+  // behind every step on every pass); the last steps (straight-line code)
+  // refill while steps remain, so nothing is in flight at the epilogue.  x
+  // alternates between two LDS buffers (the barrier of step c+1 orders step
+  // c's reads before the writes of step c+2).
+  Stage ring[3];
+#pragma unroll
+  for (int j = 0; j < 3; ++j) {
+    issue(ring[j], min(j, n_steps - 1));
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  auto step = [&](Stage& st, int c, bool refill) {
     unsigned char* buf = sx + (c & 1) * MT * kTlXStride;
     stage_x(st, buf);
     __syncthreads();
     mma_step(st, buf);
-    issue(st, min(c + 3, n_steps - 1));
+    if (refill) issue(st, c + 3);
     __builtin_amdgcn_sched_barrier(0);  // keep the requests here, ahead of the next step's wait
   };
   int c = 0;
-  for (; c + 2 < n_steps; c += 3) {  // no exit inside the body: every path around the loop issues three steps
-    step(s0, c);
-    step(s1, c + 1);
-    step(s2, c + 2);
+  for (; c + 6 <= n_steps; c += 3) {
+    step(ring[0], c, true);
+    step(ring[1], c + 1, true);
+    step(ring[2], c + 2, true);
   }
-  if (c < n_steps) {
-    step(s0, c);
-    if (c + 1 < n_steps) step(s1, c + 1);
-  }
+#pragma unroll
+  for (int j = 0; j < 5; ++j)
+    if (c + j < n_steps) step(ring[j % 3], c + j, c + j + 3 < n_steps);
 
   // logits: lane holds z[m0 + 16*MB*wm + 16*mb + lr][v0 + 16*vb + 4*lg + i]
   const bool vec_ok = (a.vocab & 3) == 0;
