@@ -179,7 +179,7 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmArgs a) {
   // step c's products, so waiting for step c never waits for newer requests.
   // (Rows shorter than the ring: the slots past the last step are requested
   // with clamped steps and never consumed.)
-  constexpr int kStages = MB == 3 ? 3 : 2;
+  constexpr int kStages = MB == 3 ? 3 : 2;  // at most 256 VGPRs: two workgroups per CU
   constexpr int XPT = XStage<MB>::kPerThread;
   static_assert(XStage<MB>::kPieces % 256 == 0, "every thread stages whole pieces of x");
   struct Stage {
@@ -300,7 +300,7 @@ constexpr int kTlXStride = kTlStep + 16;     // LDS row stride of the x tile
 constexpr int kTlRows = 128;                 // vocabulary rows per workgroup
 
 template <int MB, int KO>
-__global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
+__device__ __forceinline__ void lmhead_tiled_body(const LmArgs& a) {
   constexpr int VB = 4;                            // 16-row vocabulary blocks per wave
   constexpr int MT = 32 * MB;                      // token rows per workgroup
   constexpr int XP = MT * kTlStep / 16 / 256;      // 16-byte x pieces per thread per step
@@ -487,6 +487,11 @@ __global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
   }
 }
 
+template <int MB, int KO>
+__global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
+  lmhead_tiled_body<MB, KO>(a);
+}
+
 template <typename T, int KO>
 static hipError_t launch_mb(int mb, dim3 grid, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop) {
   const dim3 blk(256);
@@ -503,18 +508,20 @@ hipError_t launch_lmhead(int dtype, int mb, int ko, const LmArgs& a, hipStream_t
   const int n_vt = (a.vocab + kLmRows - 1) / kLmRows;
   const int n_grp = (n_vt + 7) / 8;
   dim3 grid(n_grp * 8 * a.n_mtiles);
-  if (mb == 8 || mb == 16) {  // tiled variant: MT = 128 or 256 token rows, 128-row vocabulary tiles (bf16)
+  if (mb == 6 || mb == 8 || mb == 16) {  // tiled variant: MT = 96, 128 or 256 token rows, 128-row vocabulary tiles (bf16)
     if (dtype != 1) return hipErrorInvalidValue;
     const int n_vt2 = (a.vocab + kTlRows - 1) / kTlRows;
     dim3 tgrid(((n_vt2 + 7) / 8) * 8 * a.n_mtiles);
     const dim3 blk(256);
     const int tmb = mb / 2;
     if (ko == 8)
-      return tmb == 4 ? launch_k(lmhead_tiled_kernel<4, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a)
-                      : launch_k(lmhead_tiled_kernel<8, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a);
+      return tmb == 3   ? launch_k(lmhead_tiled_kernel<3, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a)
+             : tmb == 4 ? launch_k(lmhead_tiled_kernel<4, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a)
+                        : launch_k(lmhead_tiled_kernel<8, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a);
     if (ko == 16)
-      return tmb == 4 ? launch_k(lmhead_tiled_kernel<4, 16>, tgrid, blk, 0, s, nullptr, ev_stop, a)
-                      : launch_k(lmhead_tiled_kernel<8, 16>, tgrid, blk, 0, s, nullptr, ev_stop, a);
+      return tmb == 3   ? launch_k(lmhead_tiled_kernel<3, 16>, tgrid, blk, 0, s, nullptr, ev_stop, a)
+             : tmb == 4 ? launch_k(lmhead_tiled_kernel<4, 16>, tgrid, blk, 0, s, nullptr, ev_stop, a)
+                        : launch_k(lmhead_tiled_kernel<8, 16>, tgrid, blk, 0, s, nullptr, ev_stop, a);
     return hipErrorInvalidValue;
   }
   if (ko == 8)
