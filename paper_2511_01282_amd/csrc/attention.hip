@@ -561,9 +561,7 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
     // to the matrix cores; V is written to the wave's LDS tile and read back
     // transposed.  Tile i is waited for, its scores and V^T fragments taken,
     // and tile i+2 is issued into the registers it frees, so two tiles stream
-    // while tile i is processed.  Past the last tile the issue repeats the
-    // split's last row (cache hits, results unused), which keeps the count of
-    // loads behind every tile constant.
+    // while tile i is processed.
     unsigned char* vt = s_work + (size_t)wave * kKvTile * D * 2;
     const int t_last = max(kv_hi - 1, 0);
     auto tile_row = [&](int i) { return i < n_tiles ? t_first + i * t_step : t_last; };
@@ -581,24 +579,32 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
     __builtin_amdgcn_sched_barrier(0);
     ancestor_bits<NB>(qnode, p_lo, p_hi, n_nodes, anc);  // needs the parents only, while the tiles stream
     // one tile: scores from K, V through LDS, then the tile two ahead issued into the freed registers
-    auto tile_step = [&](KTile<D>& kt, VTile<D>& vv, int i) {
+    auto tile_step = [&](KTile<D>& kt, VTile<D>& vv, int i, bool refill) {
       f32x4 s[2][NB];
       scores_bf16<D, NB>(kt, qf, s);
       store_v_bf16<D>(vv, vt, lane);
       wave_lds_sync();
       u32x4 vf[DB];
       read_vt_bf16<D>(vt, lane, vf);
-      load_k_bf16<D>(kt, kbase, tile_row(i + 2), kv_hi, lane);
-      load_v_bf16<D>(vv, vbase, tile_row(i + 2), kv_hi, lane);
+      if (refill) {
+        load_k_bf16<D>(kt, kbase, tile_row(i + 2), kv_hi, lane);
+        load_v_bf16<D>(vv, vbase, tile_row(i + 2), kv_hi, lane);
+      }
       softmax_pv_bf16<D, NB>(s, vf, t_first + i * t_step, kv_hi, L, qnode, anc, a.scale_log2, m_run, l_run, o, lane);
       wave_lds_sync();  // this tile's V^T reads precede the next tile's writes
     };
+    // Steady state: both halves refill real tiles, so the count of loads behind
+    // every tile is the same on every pass.  The last tiles (straight-line code)
+    // refill only while tiles remain: no load is left in flight for the
+    // workgroup's merge barrier to wait for.
     int i = 0;
-    for (; i + 1 < n_tiles; i += 2) {  // no exit between the halves: every path around the loop issues two tiles
-      tile_step(ka, va, i);
-      tile_step(kb, vb, i + 1);
+    for (; i + 4 <= n_tiles; i += 2) {
+      tile_step(ka, va, i, true);
+      tile_step(kb, vb, i + 1, true);
     }
-    if (i < n_tiles) tile_step(ka, va, i);
+    if (i < n_tiles) tile_step(ka, va, i, i + 2 < n_tiles);
+    if (i + 1 < n_tiles) tile_step(kb, vb, i + 1, i + 3 < n_tiles);
+    if (i + 2 < n_tiles) tile_step(ka, va, i + 2, false);
   } else {
     // float32: registers hold one tile; V is transposed through LDS by the VALU
     ancestor_bits<NB>(qnode, p_lo, p_hi, n_nodes, anc);
