@@ -21,6 +21,8 @@
 // reduces each token row's 64 logits of this workgroup to a TilePartial
 // (online-softmax statistics and the exact top-K), so the vocabulary pass never
 // re-reads the logits.
+#include <atomic>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -280,6 +282,122 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Persistent form of the same tile (large vocabularies): when the tiles
+// outnumber the workgroups that fit on the GPU at once, each resident
+// workgroup walks several tiles (ids blockIdx.x + k * gridDim.x) as one
+// stream of K steps.  The register ring runs on across tile boundaries, so the
+// next tile's first W steps are already in flight during a tile's epilogue,
+// and there is one start-up latency per workgroup instead of one per tile.
+// gridDim.x is a multiple of 8 * n_mtiles, so a workgroup keeps its M tile and
+// the M tiles of one vocabulary tile still run together on one XCD; the ids
+// past V all sit in the last group, so a workgroup's valid tiles are a prefix.
+// Requires an even number of K steps per row (two ring slots per tile).
+template <typename T, int MB, int KO>
+__global__ __launch_bounds__(256, 2) void lmhead_persistent_kernel(LmArgs a) {
+  constexpr int ES = Elem<T>::kBytes;
+  __shared__ __align__(16) unsigned char sx[2][16 * MB * kLmXStride];
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int n_mt = a.n_mtiles;
+  const int n_vt = (a.vocab + kLmRows - 1) / kLmRows;
+  const int n_ids = ((n_vt + 7) / 8) * 8 * n_mt;
+  const int G = gridDim.x;
+  auto vt_of = [&](int k) {
+    const int id = (int)blockIdx.x + k * G;
+    const int grp = id / (8 * n_mt), rem = id % (8 * n_mt);
+    return grp * 8 + rem % 8;
+  };
+  int n_my = 0;
+  while ((int)blockIdx.x + n_my * G < n_ids && vt_of(n_my) < n_vt) ++n_my;
+  if (n_my == 0) return;
+  const int mt = ((int)blockIdx.x % (8 * n_mt)) / 8;
+  const int m0 = mt * 16 * MB;
+  const size_t row_bytes = (size_t)a.hidden_size * ES;
+  const int n_steps = (int)(row_bytes / kLmChunkBytes);
+  const int total = n_my * n_steps;
+  const char* xbase = reinterpret_cast<const char*>(a.x);
+  const char* wbase = reinterpret_cast<const char*>(a.w);
+
+  constexpr int XPT = XStage<MB>::kPerThread;
+  static_assert(XStage<MB>::kPieces % 256 == 0, "every thread stages whole pieces of x");
+  struct Stage {
+    u32x4 w[kLmPieces];
+    u32x4 x[XPT];
+  };
+  // global step g = k * n_steps + s: K step s of this workgroup's k-th tile
+  // (each tile starts at its own rotated step, as in lmhead_kernel)
+  auto issue = [&](Stage& st, int g) {
+    const int k = g / n_steps, s = g - k * n_steps;
+    const int vt = vt_of(k);
+    const int rot = vt % n_steps;
+    const size_t off = (size_t)(s + rot < n_steps ? s + rot : s + rot - n_steps) * kLmChunkBytes;
+    const int v = min(vt * kLmRows + 16 * wave + lr, a.vocab - 1);  // rows past V: results not stored
+    const char* wrow = wbase + (size_t)v * row_bytes + lg * 16;
+#pragma unroll
+    for (int kp = 0; kp < kLmPieces; ++kp) st.w[kp] = ld16(wrow + off + kp * 64);
+#pragma unroll
+    for (int t = 0; t < XPT; ++t) {
+      const int idx = threadIdx.x + 256 * t;
+      const int r = idx / (kLmChunkBytes / 16), pc = idx % (kLmChunkBytes / 16);
+      const int m = min(m0 + r, a.m_rows - 1);  // rows past M: results not stored
+      st.x[t] = ld16(xbase + (size_t)m * row_bytes + off + pc * 16);
+    }
+  };
+  f32x4 acc[MB];
+  auto step = [&](Stage& st, int g) {
+    unsigned char* buf = sx[g & 1];
+#pragma unroll
+    for (int t = 0; t < XPT; ++t) {
+      const int idx = threadIdx.x + 256 * t;
+      const int r = idx / (kLmChunkBytes / 16), pc = idx % (kLmChunkBytes / 16);
+      *reinterpret_cast<u32x4*>(buf + r * kLmXStride + pc * 16) = st.x[t];
+    }
+    __syncthreads();
+    mma_step<T, MB>(acc, st.w, buf, lr, lg);
+    issue(st, min(g + 2, total - 1));  // past the last step: the last step again, unused
+    __builtin_amdgcn_sched_barrier(0);  // keep the requests here, ahead of the next step's wait
+  };
+  Stage ring[2];
+  issue(ring[0], 0);
+  __builtin_amdgcn_sched_barrier(0);
+  issue(ring[1], min(1, total - 1));
+  __builtin_amdgcn_sched_barrier(0);
+  const bool vec_ok = (a.vocab & 3) == 0;
+  for (int k = 0; k < n_my; ++k) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int g0 = k * n_steps;
+    for (int s = 0; s < n_steps; s += 2) {
+      step(ring[0], g0 + s);
+      step(ring[1], g0 + s + 1);
+    }
+    // epilogue of tile k (the next tile's first steps are already in flight)
+    const int vt = vt_of(k);
+    const int vw = vt * kLmRows + 16 * wave;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int m = m0 + 16 * mb + lr;
+      const int vv = vw + 4 * lg;
+      if (m >= a.m_rows) continue;
+      float* dst = a.logits + (size_t)m * a.vocab + vv;
+      if (vec_ok && vv + 3 < a.vocab) {
+        *reinterpret_cast<f32x4*>(dst) = acc[mb];
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (vv + i < a.vocab) dst[i] = acc[mb][i];
+      }
+    }
+    if (a.partials) {
+      __syncthreads();  // the x tiles in LDS are no longer read
+      tile_partials<MB, KO>(acc, &sx[0][0], vw, vt, m0, a, lane, wave);
+      __syncthreads();  // the statistics scratch is read before the next tile stages x
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Tiled variant for many token rows (up to 256 per pass).  With many token
 // rows the x tile, not W, dominates what a workgroup pulls through its CU, so
 // a workgroup here owns 128 vocabulary rows (each x row it loads serves twice
@@ -492,14 +610,43 @@ __global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
   lmhead_tiled_body<MB, KO>(a);
 }
 
+// Workgroups of a kernel that fit on the device at once (host occupancy
+// query, cached per kernel; 0 if the query fails).
+template <typename F>
+static int resident_wgs(F kernel) {
+  static std::atomic<int> cached{-1};
+  int v = cached.load(std::memory_order_relaxed);
+  if (v >= 0) return v;
+  int per_cu = 0, dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kernel), 256, 0) !=
+          hipSuccess)
+    v = 0;
+  else
+    v = per_cu * cus;
+  cached.store(v, std::memory_order_relaxed);
+  return v;
+}
+
+template <typename T, int MB, int KO>
+static hipError_t launch_plain(dim3 grid, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop) {
+  const dim3 blk(256);
+  const int n_steps = (int)((size_t)a.hidden_size * Elem<T>::kBytes / kLmChunkBytes);
+  const int unit = 8 * a.n_mtiles;  // the persistent grid keeps whole groups of 8 vocabulary tiles
+  const int slots = resident_wgs(lmhead_persistent_kernel<T, MB, KO>) / unit * unit;
+  if (n_steps % 2 == 0 && slots >= unit && (int)grid.x > slots)
+    return launch_k(lmhead_persistent_kernel<T, MB, KO>, dim3(slots), blk, 0, s, nullptr, ev_stop, a);
+  return launch_k(lmhead_kernel<T, MB, KO>, grid, blk, 0, s, nullptr, ev_stop, a);
+}
+
 template <typename T, int KO>
 static hipError_t launch_mb(int mb, dim3 grid, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop) {
-  const dim3 blk(256);
   switch (mb) {
-    case 1: return launch_k(lmhead_kernel<T, 1, KO>, grid, blk, 0, s, nullptr, ev_stop, a);
-    case 2: return launch_k(lmhead_kernel<T, 2, KO>, grid, blk, 0, s, nullptr, ev_stop, a);
-    case 3: return launch_k(lmhead_kernel<T, 3, KO>, grid, blk, 0, s, nullptr, ev_stop, a);
-    case 4: return launch_k(lmhead_kernel<T, 4, KO>, grid, blk, 0, s, nullptr, ev_stop, a);
+    case 1: return launch_plain<T, 1, KO>(grid, a, s, ev_stop);
+    case 2: return launch_plain<T, 2, KO>(grid, a, s, ev_stop);
+    case 3: return launch_plain<T, 3, KO>(grid, a, s, ev_stop);
+    case 4: return launch_plain<T, 4, KO>(grid, a, s, ev_stop);
     default: return hipErrorInvalidValue;
   }
 }
