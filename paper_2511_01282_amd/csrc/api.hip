@@ -150,7 +150,7 @@ respec_status respec_verify_create(const respec_verify_shape* shape, respec_veri
   p->off_pm = off; off = align256(off + prow * 4);
   p->off_pl = off; off = align256(off + prow * 4);
   p->off_x = off; off = align256(off + mcap * s.hidden * es);
-  p->off_part = off; off = align256(off + mcap * p->n_vtiles * (4 + 2 * p->ko) * 4);
+  p->off_part = off; off = align256(off + mcap * p->n_vtiles * kTileWords * 4);
   p->off_flag = off; off = align256(off + mcap * 4);
   p->n_cnt_seq = s.max_batch;
   p->off_cnt = off; off = align256(off + p->n_cnt_seq * 4);
@@ -281,7 +281,7 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
     lm.n_mtiles = cdiv(M, 16 * mb);
     lm.partials = full ? reinterpret_cast<float*>(ws + plan->off_part) : nullptr;
     lm.n_vtiles = plan->n_vtiles;
-    if (launch_lmhead(s.dtype, mb, plan->ko, lm, st, ev ? ev[2] : nullptr) != hipSuccess) return RESPEC_ERR_HIP;
+    if (launch_lmhead(s.dtype, mb, lm, st, ev ? ev[2] : nullptr) != hipSuccess) return RESPEC_ERR_HIP;
   } else if (ev && hipEventRecord(ev[2], st) != hipSuccess) {
     return RESPEC_ERR_HIP;
   }

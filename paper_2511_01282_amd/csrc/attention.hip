@@ -723,7 +723,11 @@ template <int D, bool V>
 __device__ __forceinline__ void dma_half_asm(uint32_t lds_dst, const char* base, int t0, int kv_hi, int lane) {
   constexpr int CPR = D * 2 / 16;  // 16-byte chunks per row
   constexpr int RPI = 64 / CPR;    // rows per DMA instruction (1 KB)
-  const char* tb = base + (size_t)t0 * D * 2;
+  // the tile base and the LDS destination are uniform: made scalar explicitly for the asm operands
+  const uint64_t tb_u = reinterpret_cast<uint64_t>(base + (size_t)t0 * D * 2);
+  const uint64_t tb = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(tb_u >> 32)) << 32) |
+                      (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)tb_u);
+  lds_dst = __builtin_amdgcn_readfirstlane(lds_dst);
   const bool full = t0 + kKvTile <= kv_hi;  // uniform
 #pragma unroll
   for (int q = 0; q < kKvTile / RPI; ++q) {

@@ -95,6 +95,7 @@ __device__ __forceinline__ float key_value(uint64_t k) {
 }
 __device__ __forceinline__ int key_id(uint64_t k) { return (int)(~(uint32_t)k); }
 __device__ __forceinline__ uint64_t make_key(float v, int id) {
+  v = v == 0.f ? 0.f : v;  // -0 and +0 are one value (ties go by id)
   return ((uint64_t)ord_f32(v) << 32) | (uint32_t)(~(uint32_t)id);
 }
 
@@ -193,12 +194,6 @@ __device__ __forceinline__ void merge_topk_level(uint64_t (&k)[K]) {
   merge_topk<K>(k, p);
 }
 
-// Per-tile partial of the vocabulary statistics of one token row:
-// {m, S, T, argmax, top-K keys (2 words each)}, 4 + 2K words.
-template <int K>
-struct TilePartial {
-  static constexpr int kWords = 4 + 2 * K;
-};
 
 // Cross-workgroup hand-off through global memory on a multi-XCD GPU.
 // Each XCD has its own L2, so data that one workgroup hands to another inside

@@ -36,13 +36,13 @@ struct LmArgs {
   float* logits;           // [M][V]
   int32_t m_rows, vocab, hidden_size;
   int32_t n_mtiles;        // tiles of 16*MB token rows
-  float* partials;         // [M][n_vtiles][4 + 2K] per-tile row statistics, or null
+  float* partials;         // [M][n_vtiles][4] per-tile row statistics {m, S, T, argmax}, or null
   int32_t n_vtiles;        // vocabulary tiles of 64 rows
 };
 
 struct VocabArgs {
   const float* logits;     // [M][V]
-  const float* partials;   // [M][n_vtiles][4 + 2K] written by the LM-head epilogue
+  const float* partials;   // [M][n_vtiles][4] written by the LM-head epilogue
   const int32_t* node_off; // [B+1]
   const int32_t* kv_len;   // [B]
   const int32_t* parent;
@@ -86,8 +86,13 @@ hipError_t launch_tree_attn_shared(int head_dim, int nb, int stages, dim3 grid, 
                                    const AttnArgs& a, hipStream_t s, hipEvent_t ev_start = nullptr);
 hipError_t set_tree_attn_shared_lds_limit(int head_dim, int stages, size_t lds);
 constexpr int shared_ring_bytes(int head_dim, int stages) { return stages * 2 * kKvTile * head_dim * 2; }
-hipError_t launch_lmhead(int dtype, int mb, int ko, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
+hipError_t launch_lmhead(int dtype, int mb, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
 constexpr int kLmTileRows = 64;  // vocabulary rows per LM-head workgroup (one statistics tile)
+// Per-tile partial of the vocabulary statistics of one token row over its tile
+// of 64 vocabulary rows: {m, S, T, argmax}, 16 bytes.  (m, argmax) is also the
+// tile's largest (value, id) key, from which the vocabulary pass bounds the
+// row's top-K.
+constexpr int kTileWords = 4;
 hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
 hipError_t launch_zero_i32(int32_t* p, size_t n, hipStream_t s);
 

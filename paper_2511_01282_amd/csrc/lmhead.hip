@@ -18,9 +18,9 @@
 //     same XCD at the same time and share W through that XCD's L2.
 // Output lane layout gives each lane 4 consecutive vocabulary entries of one
 // token row: 16-byte stores.  When the full step runs, the epilogue also
-// reduces each token row's 64 logits of this workgroup to a TilePartial
-// (online-softmax statistics and the exact top-K), so the vocabulary pass never
-// re-reads the logits.
+// reduces each token row's 64 logits of a statistics tile to its online-softmax
+// statistics {max, sum, entropy sum, argmax} (kTileWords), so that the
+// vocabulary pass reads them instead of the logits.
 #include <atomic>
 
 #include "common.hpp"
@@ -54,19 +54,17 @@ __device__ __forceinline__ void mma_step(f32x4 (&acc)[MB], const u32x4 (&w)[kLmP
 }
 
 // Per-row statistics of this workgroup's 64 logits of every token row, written
-// as one TilePartial: lane-local statistics and sort of 4 values, bitonic
-// top-K merges across the 4 lane groups of a row (shuffles), then across the 4
-// waves (LDS, then DPP within a quad of lanes).
-template <int MB, int KO>
+// as one tile partial {m, S, T, argmax}: lane-local statistics of 4 values,
+// merged across the 4 lane groups of a row (permlane swaps), then across the
+// 4 waves (LDS, then DPP within a quad of lanes).
+template <int MB>
 __device__ __forceinline__ void tile_partials(const f32x4 (&acc)[MB], unsigned char* lds, int vw, int vt, int m0,
                                               const LmArgs& a, int lane, int wave) {
-  constexpr int W = TilePartial<KO>::kWords;
   constexpr int ROWS = 16 * MB;
   const int lr = lane & 15, lg = lane >> 4;
-  uint32_t* s_part = reinterpret_cast<uint32_t*>(lds);  // [4 waves][ROWS][W]
+  u32x4* s_part = reinterpret_cast<u32x4*>(lds);  // [4 waves][ROWS]
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
-    uint64_t key[KO];
     float mx = kNegInf;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -77,74 +75,42 @@ __device__ __forceinline__ void tile_partials(const f32x4 (&acc)[MB], unsigned c
     st.init();
     st.m = mx;
 #pragma unroll
-    for (int i = 0; i < KO; ++i) {
+    for (int i = 0; i < 4; ++i) {
       const int col = vw + 4 * lg + i;
-      const bool ok = i < 4 && col < a.vocab;
-      key[i] = ok ? make_key(acc[mb][i & 3], col) : 0ull;
-      if (i < 4) {
-        const float d = acc[mb][i] - mx;
-        const float e = ok ? __expf(d) : 0.f;
-        st.S += e;
-        st.T += ok ? e * d : 0.f;
-        st.am = (ok && acc[mb][i] == mx) ? min(st.am, col) : st.am;
-      }
+      const bool ok = col < a.vocab;
+      const float d = acc[mb][i] - mx;
+      const float e = ok ? __expf(d) : 0.f;
+      st.S += e;
+      st.T += ok ? e * d : 0.f;
+      st.am = (ok && acc[mb][i] == mx) ? min(st.am, col) : st.am;
     }
-    // sort the first 4 keys (the rest are empty)
-    auto cas = [&](int x, int y) {
-      const bool sw = key[y] > key[x];
-      const uint64_t kx = key[x], ky = key[y];
-      key[x] = sw ? ky : kx;
-      key[y] = sw ? kx : ky;
-    };
-    cas(0, 1); cas(2, 3); cas(0, 2); cas(1, 3); cas(1, 2);
     st.merge_level<4>();  // lane groups of a row: xor 16, xor 32
-    merge_topk_level<KO, 4>(key);
     st.merge_level<5>();
-    merge_topk_level<KO, 5>(key);
-    if (lg == 0) {
-      uint32_t* dst = s_part + ((size_t)wave * ROWS + 16 * mb + lr) * W;
-      dst[0] = __float_as_uint(st.m);
-      dst[1] = __float_as_uint(st.S);
-      dst[2] = __float_as_uint(st.T);
-      dst[3] = (uint32_t)st.am;
-#pragma unroll
-      for (int i = 0; i < KO; ++i) {
-        dst[4 + 2 * i] = (uint32_t)key[i];
-        dst[5 + 2 * i] = (uint32_t)(key[i] >> 32);
-      }
-    }
+    if (lg == 0)
+      s_part[wave * ROWS + 16 * mb + lr] =
+          u32x4{__float_as_uint(st.m), __float_as_uint(st.S), __float_as_uint(st.T), (uint32_t)st.am};
   }
   __syncthreads();
-  // across the 4 waves: the 4 lanes of a quad hold one row's 4 wave lists
+  // across the 4 waves: the 4 lanes of a quad hold one row's 4 wave statistics
   for (int t = threadIdx.x; t < 4 * ROWS; t += blockDim.x) {
     const int r = t >> 2, q = t & 3;
     const int m = m0 + r;
     if (m >= a.m_rows) continue;  // uniform over the quad
-    const uint32_t* src = s_part + ((size_t)q * ROWS + r) * W;
+    const u32x4 w = s_part[q * ROWS + r];
     RowStats st;
-    st.m = __uint_as_float(src[0]);
-    st.S = __uint_as_float(src[1]);
-    st.T = __uint_as_float(src[2]);
-    st.am = (int)src[3];
-    uint64_t key[KO];
-#pragma unroll
-    for (int i = 0; i < KO; ++i) key[i] = ((uint64_t)src[5 + 2 * i] << 32) | src[4 + 2 * i];
+    st.m = __uint_as_float(w[0]);
+    st.S = __uint_as_float(w[1]);
+    st.T = __uint_as_float(w[2]);
+    st.am = (int)w[3];
     st.merge_level<0>();
-    merge_topk_level<KO, 0>(key);
     st.merge_level<1>();
-    merge_topk_level<KO, 1>(key);
-    if (q == 0) {
-      u32x4* dst = reinterpret_cast<u32x4*>(a.partials + ((size_t)m * a.n_vtiles + vt) * W);
-      dst[0] = u32x4{__float_as_uint(st.m), __float_as_uint(st.S), __float_as_uint(st.T), (uint32_t)st.am};
-#pragma unroll
-      for (int i = 0; i < KO; i += 2)
-        dst[1 + i / 2] = u32x4{(uint32_t)key[i], (uint32_t)(key[i] >> 32), (uint32_t)key[i + 1],
-                               (uint32_t)(key[i + 1] >> 32)};
-    }
+    if (q == 0)
+      *reinterpret_cast<u32x4*>(a.partials + ((size_t)m * a.n_vtiles + vt) * kTileWords) =
+          u32x4{__float_as_uint(st.m), __float_as_uint(st.S), __float_as_uint(st.T), (uint32_t)st.am};
   }
 }
 
-template <typename T, int MB, int KO>
+template <typename T, int MB>
 __global__ __launch_bounds__(256) void lmhead_kernel(LmArgs a) {
   constexpr int ES = Elem<T>::kBytes;
   __shared__ __align__(16) unsigned char sx[2][16 * MB * kLmXStride];
@@ -277,7 +243,7 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmArgs a) {
   }
   if (a.partials) {
     __syncthreads();  // the x tiles in LDS are no longer read
-    tile_partials<MB, KO>(acc, &sx[0][0], vw, vt, m0, a, lane, wave);
+    tile_partials<MB>(acc, &sx[0][0], vw, vt, m0, a, lane, wave);
   }
 }
 
@@ -292,7 +258,7 @@ __global__ __launch_bounds__(256) void lmhead_kernel(LmArgs a) {
 // the M tiles of one vocabulary tile still run together on one XCD; the ids
 // past V all sit in the last group, so a workgroup's valid tiles are a prefix.
 // Requires an even number of K steps per row (two ring slots per tile).
-template <typename T, int MB, int KO>
+template <typename T, int MB>
 __global__ __launch_bounds__(256, 2) void lmhead_persistent_kernel(LmArgs a) {
   constexpr int ES = Elem<T>::kBytes;
   __shared__ __align__(16) unsigned char sx[2][16 * MB * kLmXStride];
@@ -391,7 +357,7 @@ __global__ __launch_bounds__(256, 2) void lmhead_persistent_kernel(LmArgs a) {
     }
     if (a.partials) {
       __syncthreads();  // the x tiles in LDS are no longer read
-      tile_partials<MB, KO>(acc, &sx[0][0], vw, vt, m0, a, lane, wave);
+      tile_partials<MB>(acc, &sx[0][0], vw, vt, m0, a, lane, wave);
       __syncthreads();  // the statistics scratch is read before the next tile stages x
     }
   }
@@ -417,12 +383,11 @@ constexpr int kTlPieces = kTlStep / 64;      // mma_k64 calls per K step
 constexpr int kTlXStride = kTlStep + 16;     // LDS row stride of the x tile
 constexpr int kTlRows = 128;                 // vocabulary rows per workgroup
 
-template <int MB, int KO>
+template <int MB>
 __device__ __forceinline__ void lmhead_tiled_body(const LmArgs& a) {
   constexpr int VB = 4;                            // 16-row vocabulary blocks per wave
   constexpr int MT = 32 * MB;                      // token rows per workgroup
   constexpr int XP = MT * kTlStep / 16 / 256;      // 16-byte x pieces per thread per step
-  constexpr int W = TilePartial<KO>::kWords;
   __shared__ __align__(16) unsigned char sx[2 * MT * kTlXStride];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -560,14 +525,8 @@ __device__ __forceinline__ void lmhead_tiled_body(const LmArgs& a) {
     RowStats st;
     st.init();
     st.m = mx;
-    uint64_t key[KO];
 #pragma unroll
-    for (int i = 0; i < KO; ++i) key[i] = 0ull;
-#pragma unroll
-    for (int vb = 0; vb < VB; ++vb) {
-      uint64_t kb[KO];
-#pragma unroll
-      for (int i = 0; i < KO; ++i) kb[i] = 0ull;
+    for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int col = v0 + 16 * vb + 4 * lg + i;
@@ -577,37 +536,19 @@ __device__ __forceinline__ void lmhead_tiled_body(const LmArgs& a) {
         st.S += e;
         st.T += ok ? e * d : 0.f;
         st.am = (ok && acc[vb][mb][i] == mx) ? min(st.am, col) : st.am;
-        kb[i] = ok ? make_key(acc[vb][mb][i], col) : 0ull;
       }
-      // sort this block's 4 keys, then merge them into the lane's list
-      auto cas = [&](int x, int y) {
-        const bool sw = kb[y] > kb[x];
-        const uint64_t kx = kb[x], ky = kb[y];
-        kb[x] = sw ? ky : kx;
-        kb[y] = sw ? kx : ky;
-      };
-      cas(0, 1); cas(2, 3); cas(0, 2); cas(1, 3); cas(1, 2);
-      merge_topk<KO>(key, kb);
-    }
     st.merge_level<4>();  // lane groups of a token row: xor 16, xor 32
-    merge_topk_level<KO, 4>(key);
     st.merge_level<5>();
-    merge_topk_level<KO, 5>(key);
     const int m = m0 + MB * 16 * wm + 16 * mb + lr;
-    if (lg == 0 && m < a.m_rows) {
-      u32x4* dst = reinterpret_cast<u32x4*>(a.partials + ((size_t)m * a.n_vtiles + stat_tile) * W);
-      dst[0] = u32x4{__float_as_uint(st.m), __float_as_uint(st.S), __float_as_uint(st.T), (uint32_t)st.am};
-#pragma unroll
-      for (int i = 0; i < KO; i += 2)
-        dst[1 + i / 2] = u32x4{(uint32_t)key[i], (uint32_t)(key[i] >> 32), (uint32_t)key[i + 1],
-                               (uint32_t)(key[i + 1] >> 32)};
-    }
+    if (lg == 0 && m < a.m_rows)
+      *reinterpret_cast<u32x4*>(a.partials + ((size_t)m * a.n_vtiles + stat_tile) * kTileWords) =
+          u32x4{__float_as_uint(st.m), __float_as_uint(st.S), __float_as_uint(st.T), (uint32_t)st.am};
   }
 }
 
-template <int MB, int KO>
+template <int MB>
 __global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
-  lmhead_tiled_body<MB, KO>(a);
+  lmhead_tiled_body<MB>(a);
 }
 
 // Workgroups of a kernel that fit on the device at once (host occupancy
@@ -629,29 +570,29 @@ static int resident_wgs(F kernel) {
   return v;
 }
 
-template <typename T, int MB, int KO>
+template <typename T, int MB>
 static hipError_t launch_plain(dim3 grid, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop) {
   const dim3 blk(256);
   const int n_steps = (int)((size_t)a.hidden_size * Elem<T>::kBytes / kLmChunkBytes);
   const int unit = 8 * a.n_mtiles;  // the persistent grid keeps whole groups of 8 vocabulary tiles
-  const int slots = resident_wgs(lmhead_persistent_kernel<T, MB, KO>) / unit * unit;
+  const int slots = resident_wgs(lmhead_persistent_kernel<T, MB>) / unit * unit;
   if (n_steps % 2 == 0 && slots >= unit && (int)grid.x > slots)
-    return launch_k(lmhead_persistent_kernel<T, MB, KO>, dim3(slots), blk, 0, s, nullptr, ev_stop, a);
-  return launch_k(lmhead_kernel<T, MB, KO>, grid, blk, 0, s, nullptr, ev_stop, a);
+    return launch_k(lmhead_persistent_kernel<T, MB>, dim3(slots), blk, 0, s, nullptr, ev_stop, a);
+  return launch_k(lmhead_kernel<T, MB>, grid, blk, 0, s, nullptr, ev_stop, a);
 }
 
-template <typename T, int KO>
+template <typename T>
 static hipError_t launch_mb(int mb, dim3 grid, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop) {
   switch (mb) {
-    case 1: return launch_plain<T, 1, KO>(grid, a, s, ev_stop);
-    case 2: return launch_plain<T, 2, KO>(grid, a, s, ev_stop);
-    case 3: return launch_plain<T, 3, KO>(grid, a, s, ev_stop);
-    case 4: return launch_plain<T, 4, KO>(grid, a, s, ev_stop);
+    case 1: return launch_plain<T, 1>(grid, a, s, ev_stop);
+    case 2: return launch_plain<T, 2>(grid, a, s, ev_stop);
+    case 3: return launch_plain<T, 3>(grid, a, s, ev_stop);
+    case 4: return launch_plain<T, 4>(grid, a, s, ev_stop);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_lmhead(int dtype, int mb, int ko, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop) {
+hipError_t launch_lmhead(int dtype, int mb, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop) {
   const int n_vt = (a.vocab + kLmRows - 1) / kLmRows;
   const int n_grp = (n_vt + 7) / 8;
   dim3 grid(n_grp * 8 * a.n_mtiles);
@@ -661,21 +602,11 @@ hipError_t launch_lmhead(int dtype, int mb, int ko, const LmArgs& a, hipStream_t
     dim3 tgrid(((n_vt2 + 7) / 8) * 8 * a.n_mtiles);
     const dim3 blk(256);
     const int tmb = mb / 2;
-    if (ko == 8)
-      return tmb == 3   ? launch_k(lmhead_tiled_kernel<3, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a)
-             : tmb == 4 ? launch_k(lmhead_tiled_kernel<4, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a)
-                        : launch_k(lmhead_tiled_kernel<8, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a);
-    if (ko == 16)
-      return tmb == 3   ? launch_k(lmhead_tiled_kernel<3, 16>, tgrid, blk, 0, s, nullptr, ev_stop, a)
-             : tmb == 4 ? launch_k(lmhead_tiled_kernel<4, 16>, tgrid, blk, 0, s, nullptr, ev_stop, a)
-                        : launch_k(lmhead_tiled_kernel<8, 16>, tgrid, blk, 0, s, nullptr, ev_stop, a);
-    return hipErrorInvalidValue;
+    return tmb == 3   ? launch_k(lmhead_tiled_kernel<3>, tgrid, blk, 0, s, nullptr, ev_stop, a)
+           : tmb == 4 ? launch_k(lmhead_tiled_kernel<4>, tgrid, blk, 0, s, nullptr, ev_stop, a)
+                      : launch_k(lmhead_tiled_kernel<8>, tgrid, blk, 0, s, nullptr, ev_stop, a);
   }
-  if (ko == 8)
-    return dtype == 1 ? launch_mb<bf16_t, 8>(mb, grid, a, s, ev_stop) : launch_mb<float, 8>(mb, grid, a, s, ev_stop);
-  if (ko == 16)
-    return dtype == 1 ? launch_mb<bf16_t, 16>(mb, grid, a, s, ev_stop) : launch_mb<float, 16>(mb, grid, a, s, ev_stop);
-  return hipErrorInvalidValue;
+  return dtype == 1 ? launch_mb<bf16_t>(mb, grid, a, s, ev_stop) : launch_mb<float>(mb, grid, a, s, ev_stop);
 }
 
 }  // namespace respec

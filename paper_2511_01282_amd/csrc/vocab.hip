@@ -2,10 +2,12 @@
 //
 // Per node row i (ReSpec: entropy of Eq. 1; relaxed check of Eq. 6-7;
 // look-ahead tolerance of Section 3.4; winner of Algorithm 1's RelaxedVerify):
-//   1. one workgroup merges the row's per-tile partials written by the LM-head
-//      epilogue (online max / sum / entropy terms and exact top-K lists) with
-//      bitonic list merges: lse = m + log S, entropy = log S - T/S, top-k by
-//      (z desc, id asc); then, for every child j of node i, the predicates of
+//   1. one workgroup merges the row's per-tile statistics written by the
+//      LM-head epilogue (online max / sum / entropy terms and the tile's
+//      (max, argmax)): lse = m + log S, entropy = log S - T/S; the row's top-K
+//      entries lie in the tiles with the K largest maxima, so only those are
+//      read back to give the exact top-k by (z desc, id asc); then, for every
+//      child j of node i, the predicates of
 //      j's token: GREEDY (t == argmax), TOPK (t among the first k), TAU
 //      (z_max - z_t <= tau, compared in double), RELAXED (retrieved and TOPK and
 //      TAU);
@@ -17,8 +19,9 @@
 //      and walks its leaf chains before taking the ticket (that needs only the
 //      parents), so the winner of the ticket only reads the predicates.
 // A row is reduced by four waves (one when the vocabulary has at most 64
-// tiles): each wave reduces its lanes' partials by wave-wide reductions and a
-// top-K by repeated maxima, then wave 0 combines the waves.
+// tiles): each wave reduces its lanes' statistics by wave-wide reductions,
+// picks its K largest tile maxima by repeated maxima, reads those tiles and
+// takes their top-K the same way; then wave 0 combines the waves.
 // Extra workgroups (one per sequence) report sequences whose node range is
 // unusable, since no row workgroup would finish them.
 #include "common.hpp"
@@ -68,6 +71,34 @@ __device__ __forceinline__ void wave_topk(uint64_t (&key)[L], uint64_t (&top)[K]
     for (int k = 0; k + 1 < L; ++k) key[k] = pop ? key[k + 1] : key[k];
     key[L - 1] = pop ? 0ull : key[L - 1];
   }
+}
+
+// Descending sort of a thread's N keys (bitonic network, N a power of two).
+template <int N>
+__device__ __forceinline__ void sort_desc(uint64_t (&k)[N]) {
+#pragma unroll
+  for (int sz = 2; sz <= N; sz *= 2)
+#pragma unroll
+    for (int j = sz / 2; j > 0; j /= 2)
+#pragma unroll
+      for (int x = 0; x < N; ++x) {
+        const int y = x ^ j;
+        if (y > x) {
+          const bool desc = (x & sz) == 0;  // the last stage (sz = N) sorts all of it descending
+          const bool sw = desc ? k[y] > k[x] : k[x] > k[y];
+          const uint64_t kx = k[x], ky = k[y];
+          k[x] = sw ? ky : kx;
+          k[y] = sw ? kx : ky;
+        }
+      }
+}
+
+// Insert key v into a descending list of N keys, dropping the smallest.
+template <int N>
+__device__ __forceinline__ void insert_desc(uint64_t (&k)[N], uint64_t v) {
+#pragma unroll
+  for (int x = N - 1; x > 0; --x) k[x] = v > k[x - 1] ? k[x - 1] : (v > k[x] ? v : k[x]);
+  k[0] = v > k[0] ? v : k[0];
 }
 
 // Softmax statistics of the wave's union of disjoint sets: the maximum first,
@@ -328,12 +359,11 @@ struct FinalizeLds {
 };
 
 // One node row: statistics, children's predicates, and (last row of the
-// sequence) the path.  WPR waves reduce the row (1 or 4).  Wide: batch >= 64
-// (node offsets in several groups).
-template <int KO, int WPR, bool Wide>
+// sequence) the path.  WPR waves reduce the row (1 or 4); each thread keeps
+// the keys of up to LB tiles.  Wide: batch >= 64 (node offsets in several
+// groups).
+template <int KO, int WPR, int LB, bool Wide>
 __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>& sh) {
-  constexpr int W = TilePartial<KO>::kWords;
-  constexpr int kLoadBatch = WPR == 1 ? 1 : 8;  // tile partials per thread requested up front
   constexpr int NT = 64 * WPR;   // threads of the row
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int tid = threadIdx.x;
@@ -343,15 +373,14 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
   // thread's tile partials, then (once the sequence is known) the parent, token
   // and tag of nodes tid and tid + NT.  All are issued by every lane with
   // clamped indices, so the load counts are the same on every path.
-  const uint32_t* prow = reinterpret_cast<const uint32_t*>(a.partials) + (size_t)i * a.n_vtiles * W;
-  u32x4 buf[kLoadBatch][W / 4];
+  const u32x4* prow = reinterpret_cast<const u32x4*>(a.partials) + (size_t)i * a.n_vtiles;
+  u32x4 buf[LB];
   int v0, vn0;
   load_offsets(a, lane, v0, vn0);
 #pragma unroll
-  for (int u = 0; u < kLoadBatch; ++u) {
+  for (int u = 0; u < LB; ++u) {
     const int t = min(tid + u * NT, a.n_vtiles - 1);
-#pragma unroll
-    for (int q = 0; q < W / 4; ++q) buf[u][q] = *reinterpret_cast<const u32x4*>(prow + (size_t)t * W + 4 * q);
+    buf[u] = prow[t];
   }
   const SeqLayout lay = scan_layout<Wide>(a, i, lane, v0, vn0);
   const bool lay_ok = lay.ok;
@@ -368,41 +397,25 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
   }
   const int kv_b = a.kv_len[lay_ok ? b : 0];
 
-  // fold the row's tile partials: this thread's tiles (the first is taken as it is)
+  // Fold the row's tile statistics (this thread's tiles), and keep each tile's
+  // largest (value, id) key; the id's tile is the tile.
   RowStats st;
   st.init();
-  uint64_t key[KO];
+  uint64_t tk[LB];  // this thread's tile keys, descending after the sort below
 #pragma unroll
-  for (int k = 0; k < KO; ++k) key[k] = 0ull;
-  auto unpack = [&](const u32x4 (&pb)[W / 4], uint64_t (&pk)[KO]) {
-#pragma unroll
-    for (int k = 0; k < KO; ++k) {
-      const u32x4 w4 = pb[1 + k / 2];
-      pk[k] = (k & 1) ? (((uint64_t)w4[3] << 32) | w4[2]) : (((uint64_t)w4[1] << 32) | w4[0]);
-    }
-  };
-  auto fold = [&](const u32x4 (&pb)[W / 4]) {
-    st.merge(__uint_as_float(pb[0][0]), __uint_as_float(pb[0][1]), __uint_as_float(pb[0][2]), (int)pb[0][3]);
-    uint64_t pk[KO];
-    unpack(pb, pk);
-    merge_topk<KO>(key, pk);
-  };
-  if (tid < a.n_vtiles) {
-    st.m = __uint_as_float(buf[0][0][0]);
-    st.S = __uint_as_float(buf[0][0][1]);
-    st.T = __uint_as_float(buf[0][0][2]);
-    st.am = (int)buf[0][0][3];
-    unpack(buf[0], key);
+  for (int u = 0; u < LB; ++u) {
+    const bool ok = tid + u * NT < a.n_vtiles;
+    const float m_t = __uint_as_float(buf[u][0]);
+    const int am_t = (int)buf[u][3];
+    if (ok) st.merge(m_t, __uint_as_float(buf[u][1]), __uint_as_float(buf[u][2]), am_t);
+    tk[u] = ok ? make_key(m_t, am_t) : 0ull;
   }
-#pragma unroll
-  for (int u = 1; u < kLoadBatch; ++u)
-    if (tid + u * NT < a.n_vtiles) fold(buf[u]);
-  for (int t = tid + kLoadBatch * NT; t < a.n_vtiles; t += NT) {
-    u32x4 pb[W / 4];
-#pragma unroll
-    for (int q = 0; q < W / 4; ++q) pb[q] = *reinterpret_cast<const u32x4*>(prow + (size_t)t * W + 4 * q);
-    fold(pb);
+  const bool spill = a.n_vtiles > LB * NT;  // (uniform) tiles past the key lists: read the whole row
+  for (int t = tid + LB * NT; t < a.n_vtiles; t += NT) {
+    const u32x4 pb = prow[t];
+    st.merge(__uint_as_float(pb[0]), __uint_as_float(pb[1]), __uint_as_float(pb[2]), (int)pb[3]);
   }
+  sort_desc<LB>(tk);
   // the children of node li request their logit z_li[t] now (the parents have had time to arrive)
   bool is_child[NPT], tok_ok[NPT];
   float c_z[NPT];
@@ -413,10 +426,32 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
     tok_ok[u] = c_tok[u] >= 0 && c_tok[u] < a.vocab;
     c_z[u] = a.logits[(size_t)i * a.vocab + (is_child[u] && tok_ok[u] ? c_tok[u] : 0)];
   }
-  // the wave: statistics by reductions, top-K by repeated maxima
-  wave_rowstats(st);
+  // The K largest tile keys of the wave.  Keys are distinct, so an entry of
+  // the row's top-K that lies in one of this wave's tiles lies in one of these
+  // K tiles (else K tile maxima of the wave would all exceed it).  The wave
+  // reads those tiles whole (64/K lanes per tile, K columns per lane) and takes
+  // their top-K; the row's top-K is the top-K of the waves' lists.
   uint64_t top[KO];
-  wave_topk<KO, KO>(key, top);
+  wave_topk<LB, KO>(tk, top);
+  const float* zrow = a.logits + (size_t)i * a.vocab;
+  uint64_t ck[KO];
+  if (!spill) {
+    constexpr int LPT = 64 / KO;  // lanes per candidate tile
+    uint64_t mine = top[0];
+#pragma unroll
+    for (int k = 1; k < KO; ++k) mine = lane / LPT == k ? top[k] : mine;
+    const uint32_t tile = mine ? (uint32_t)key_id(mine) / kLmTileRows : 0xFFFFFFFFu;
+    const int col0 = tile < (uint32_t)a.n_vtiles ? (int)tile * kLmTileRows + lane % LPT : a.vocab;
+    float z[KO];
+#pragma unroll
+    for (int e = 0; e < KO; ++e) z[e] = col0 + LPT * e < a.vocab ? zrow[col0 + LPT * e] : 0.f;
+#pragma unroll
+    for (int e = 0; e < KO; ++e) ck[e] = col0 + LPT * e < a.vocab ? make_key(z[e], col0 + LPT * e) : 0ull;
+  } else {
+#pragma unroll
+    for (int k = 0; k < KO; ++k) ck[k] = 0ull;
+    for (int col = tid; col < a.vocab; col += NT) insert_desc<KO>(ck, make_key(zrow[col], col));
+  }
   // the sequence's nodes go to LDS (the path reduction reads them)
   if (lay_ok) {
 #pragma unroll
@@ -429,6 +464,8 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
       }
     }
   }
+  // the wave's statistics (by reductions) while the candidate logits arrive
+  wave_rowstats(st);
   if constexpr (WPR > 1) {
     if (lane == 0) {
       sh.st[wave][0] = st.m;
@@ -436,6 +473,10 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
       sh.st[wave][2] = st.T;
       sh.st[wave][3] = __int_as_float(st.am);
     }
+  }
+  sort_desc<KO>(ck);
+  wave_topk<KO, KO>(ck, top);
+  if constexpr (WPR > 1) {
     if (lane < KO) {
       uint64_t mine = top[0];
 #pragma unroll
@@ -456,6 +497,7 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
       wave_topk<1, KO>(k1, top);
     }
   }
+  uint64_t key[KO];
 #pragma unroll
   for (int k = 0; k < KO; ++k) key[k] = top[k];
   // row results: LDS for the predicates, memory for the outputs (wave 0)
@@ -530,7 +572,7 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
   if (lane == 0) st_dev(a.seq_counter + b, 0);
 }
 
-template <int KO, int WPR>
+template <int KO, int WPR, int LB>
 __global__ __launch_bounds__(64 * WPR) void finalize_kernel(VocabArgs a) {
   __shared__ FinalizeLds<KO> sh;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -546,18 +588,25 @@ __global__ __launch_bounds__(64 * WPR) void finalize_kernel(VocabArgs a) {
     return;
   }
   if (a.batch < 64)
-    finalize_row<KO, WPR, false>(a, sh);
+    finalize_row<KO, WPR, LB, false>(a, sh);
   else
-    finalize_row<KO, WPR, true>(a, sh);
+    finalize_row<KO, WPR, LB, true>(a, sh);
+}
+
+template <int KO>
+hipError_t launch_finalize_ko(int blocks, const VocabArgs& a, hipStream_t s, hipEvent_t ev_stop) {
+  // one wave per row up to 64 vocabulary tiles, else four, with the smallest
+  // per-thread key list that holds every tile (beyond 4096 tiles the rows are
+  // read whole)
+  if (a.n_vtiles <= 64) return launch_k(finalize_kernel<KO, 1, 1>, dim3(blocks), dim3(64), 0, s, nullptr, ev_stop, a);
+  if (a.n_vtiles <= 512) return launch_k(finalize_kernel<KO, 4, 2>, dim3(blocks), dim3(256), 0, s, nullptr, ev_stop, a);
+  if (a.n_vtiles <= 2048) return launch_k(finalize_kernel<KO, 4, 8>, dim3(blocks), dim3(256), 0, s, nullptr, ev_stop, a);
+  return launch_k(finalize_kernel<KO, 4, 16>, dim3(blocks), dim3(256), 0, s, nullptr, ev_stop, a);
 }
 
 hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s, hipEvent_t ev_stop) {
-  // one wave per row up to 64 vocabulary tiles, else four
-  const bool one = a.n_vtiles <= 64;
-  if (ko == 8 && one) return launch_k(finalize_kernel<8, 1>, dim3(blocks), dim3(64), 0, s, nullptr, ev_stop, a);
-  if (ko == 8) return launch_k(finalize_kernel<8, 4>, dim3(blocks), dim3(256), 0, s, nullptr, ev_stop, a);
-  if (ko == 16 && one) return launch_k(finalize_kernel<16, 1>, dim3(blocks), dim3(64), 0, s, nullptr, ev_stop, a);
-  if (ko == 16) return launch_k(finalize_kernel<16, 4>, dim3(blocks), dim3(256), 0, s, nullptr, ev_stop, a);
+  if (ko == 8) return launch_finalize_ko<8>(blocks, a, s, ev_stop);
+  if (ko == 16) return launch_finalize_ko<16>(blocks, a, s, ev_stop);
   return hipErrorInvalidValue;
 }
 

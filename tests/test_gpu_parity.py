@@ -124,6 +124,39 @@ def test_edge_case_parity(rt, name):
     compare(case, rt.run(case.w), f"edge {name}")
 
 
+# Vocabulary sizes that take each form of the vocabulary pass: one wave per row
+# (<= 64 tiles of 64 tokens), four waves with 2, 8 and 16 tile keys per thread,
+# and rows read whole (more than 4096 tiles).  "clustered" gives 24
+# consecutive tokens (across a tile boundary) near-copies of one LM-head row
+# scaled by 6-7.2, so that on many rows most of the top-k sits in one tile.
+VOCAB_TIERS = [
+    (3000, 16, True),
+    (30000, 8, True),
+    (70000, 8, False),
+    (200000, 16, True),
+    (300000, 8, True),
+]
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("vocab,topk_out,clustered", VOCAB_TIERS)
+def test_vocab_tier_parity(rt, vocab, topk_out, clustered):
+    parents = [[-1, 0, 1, 1, 3, 0], [-1, 0, 0, 2]]
+    shp = synth.Shape("edge", "bf16", 4 * 64, 4, 1, 64, vocab, 2, 6, 8, topk_out)
+    w = synth.custom(shp, parents, [70, 40], seed=211, poison_tail=True)
+    if clustered:
+        W = synth.bf16_bits_to_f32(w.lm_head).reshape(vocab, -1).copy()
+        c0 = 64 * 5 + 48
+        for k in range(24):
+            W[c0 + k] = W[7] * (6.0 + 0.05 * k) + 0.002 * W[100 + k]
+        w.lm_head = synth.f32_to_bf16_bits(W).reshape(w.lm_head.shape)
+    w.params = synth.AcceptParams(topk=topk_out, tau=1.0, min_lookahead=1, max_relaxed=2)
+    _say(f"[vocab {vocab} k={topk_out} clustered={clustered}] building")
+    case = workload.finish(w)
+    _say(f"[vocab {vocab} k={topk_out} clustered={clustered}] running GPU step")
+    compare(case, rt.run(case.w), f"vocab {vocab}")
+
+
 def _depth(parent):
     d = [0] * len(parent)
     for j in range(1, len(parent)):
