@@ -456,23 +456,24 @@ __device__ __forceinline__ void ancestor_bits(const int (&qnode)[NB], int p_lo, 
     x[nb] = qnode[nb];
     anc[nb] = u32x4{0u, 0u, 0u, 0u};
   }
+  const bool two = n_nodes > 64;  // (uniform) parents of nodes 64.. are needed
   for (int step = 0; step < kMaxNodes; ++step) {
     bool any = false;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const int xv = x[nb];
-      if (xv >= 0) {
-        const uint32_t bit = 1u << (xv & 31);
-        const int w = xv >> 5;
-        anc[nb][0] |= w == 0 ? bit : 0u;
-        anc[nb][1] |= w == 1 ? bit : 0u;
-        anc[nb][2] |= w == 2 ? bit : 0u;
-        anc[nb][3] |= w == 3 ? bit : 0u;
-      }
+      const uint32_t bit = xv >= 0 ? 1u << (xv & 31) : 0u;
+      const int w = xv >> 5;
+      anc[nb][0] |= w == 0 ? bit : 0u;
+      anc[nb][1] |= w == 1 ? bit : 0u;
+      anc[nb][2] |= w == 2 ? bit : 0u;
+      anc[nb][3] |= w == 3 ? bit : 0u;
       const int sel = (xv & 63) << 2;
-      const int pl = __builtin_amdgcn_ds_bpermute(sel, p_lo);
-      const int ph = __builtin_amdgcn_ds_bpermute(sel, p_hi);
-      const int p = xv >= 64 ? ph : pl;
+      int p = __builtin_amdgcn_ds_bpermute(sel, p_lo);
+      if (two) {
+        const int ph = __builtin_amdgcn_ds_bpermute(sel, p_hi);
+        p = xv >= 64 ? ph : p;
+      }
       x[nb] = (xv > 0 && p >= 0 && p < xv) ? p : -1;
       any |= x[nb] >= 0;
     }
@@ -577,7 +578,12 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
     load_k_bf16<D>(kb, kbase, tile_row(1), kv_hi, lane);
     load_v_bf16<D>(vb, vbase, tile_row(1), kv_hi, lane);
     __builtin_amdgcn_sched_barrier(0);
-    ancestor_bits<NB>(qnode, p_lo, p_hi, n_nodes, anc);  // needs the parents only, while the tiles stream
+    // the tree's own rows (L..) need the ancestor masks: only a split that reaches them
+    // waits for the parents (uniform)
+    if (kv_hi > L)
+      ancestor_bits<NB>(qnode, p_lo, p_hi, n_nodes, anc);
+    else
+      for (int nb = 0; nb < NB; ++nb) anc[nb] = u32x4{0u, 0u, 0u, 0u};
     // one tile: scores from K, V through LDS, then the tile two ahead issued into the freed registers
     auto tile_step = [&](KTile<D>& kt, VTile<D>& vv, int i, bool refill) {
       f32x4 s[2][NB];
@@ -607,7 +613,10 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
     if (i + 2 < n_tiles) tile_step(ka, va, i + 2, false);
   } else {
     // float32: registers hold one tile; V is transposed through LDS by the VALU
-    ancestor_bits<NB>(qnode, p_lo, p_hi, n_nodes, anc);
+    if (kv_hi > L)
+      ancestor_bits<NB>(qnode, p_lo, p_hi, n_nodes, anc);
+    else
+      for (int nb = 0; nb < NB; ++nb) anc[nb] = u32x4{0u, 0u, 0u, 0u};
     T* vt = reinterpret_cast<T*>(s_work + (size_t)wave * D * VTS * ES);
     AttnTile<T, D> ta;
     for (int i = 0; i < n_tiles; ++i) {
@@ -787,8 +796,8 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
   const int t_last = max(kv_hi - 1, 0);
   auto tile_row = [&](int i) { return i < n_tiles ? kv_lo + i * kKvTile : t_last; };
 
-  const int p_lo = a.parent[node0 + min(lane, n_nodes - 1)];
-  const int p_hi = a.parent[node0 + min(lane + 64, n_nodes - 1)];
+  int p_lo = a.parent[node0 + min(lane, n_nodes - 1)];
+  int p_hi = a.parent[node0 + min(lane + 64, n_nodes - 1)];
   const int row_wave = row_wg + wave * RB;
   u32x4 qf[NB][KCH];
   int qnode[NB];
@@ -809,6 +818,15 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
     }
   }
 
+  // Every wave has its parents and queries before the first requests are
+  // issued: the compiler's wait counts do not see the requests, so a value
+  // loaded before them and used after them would be waited for behind every
+  // request in flight (and the wait is shared by the waves that issue none).
+  asm volatile("" : "+v"(p_lo), "+v"(p_hi));
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int kc = 0; kc < KCH; ++kc) asm volatile("" : "+v"(qf[nb][kc]));
   // the first S - 1 tiles (kv_hi >= 1, so every clamped row is a valid cache row)
   if (wave < 2) {
 #pragma unroll
@@ -830,7 +848,10 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
     for (int db = 0; db < DB; ++db) o[db][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
   u32x4 anc[NB];
-  ancestor_bits<NB>(qnode, p_lo, p_hi, n_nodes, anc);
+  if (kv_hi > L)  // (uniform) only a split that reaches the tree's own rows needs the masks
+    ancestor_bits<NB>(qnode, p_lo, p_hi, n_nodes, anc);
+  else
+    for (int nb = 0; nb < NB; ++nb) anc[nb] = u32x4{0u, 0u, 0u, 0u};
   // row blocks of this wave that hold a live row (blocks past the group's last row are skipped)
   const int nbc = __builtin_amdgcn_readfirstlane(min(NB, max(0, (R - row_wave + 15) / 16)));
 
