@@ -101,6 +101,83 @@ __device__ __forceinline__ void insert_desc(uint64_t (&k)[N], uint64_t v) {
   k[0] = v > k[0] ? v : k[0];
 }
 
+// Value held by lane (lane ^ J), J a power of two up to 32: DPP row moves
+// give xor 1 and xor 2; xor 4 is xor 3 (quad reversal) followed by the mirror
+// within 8 (xor 7), xor 8 the mirror within 8 followed by the mirror within 16
+// (xor 15); xor 16 and 32 are the row swaps.
+template <int J>
+__device__ __forceinline__ int lane_xor(int v) {
+  if constexpr (J == 1) return xchg<0>(v);
+  if constexpr (J == 2) return xchg<1>(v);
+  if constexpr (J == 4) return xchg<2>(__builtin_amdgcn_mov_dpp(v, 0x1B, 0xF, 0xF, false));  // quad_perm 3,2,1,0
+  if constexpr (J == 8) return xchg<3>(xchg<2>(v));
+  if constexpr (J == 16) return xchg<4>(v);
+  return xchg<5>(v);
+}
+template <int J>
+__device__ __forceinline__ uint64_t lane_xor(uint64_t v) {
+  const uint32_t lo = (uint32_t)lane_xor<J>((int)(uint32_t)v), hi = (uint32_t)lane_xor<J>((int)(uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// One compare-exchange stage of a bitonic network over the 64 lanes: blocks
+// of S lanes, partner lane ^ J; a block is ordered descending when lane & S
+// is 0, so the last stages (S = 64) order the whole wave descending.
+template <int S, int J>
+__device__ __forceinline__ uint64_t bitonic_stage(uint64_t k, int lane) {
+  const uint64_t o = lane_xor<J>(k);
+  const bool desc = (lane & S) == 0;
+  const bool keep_max = ((lane & J) == 0) == desc;
+  const uint64_t mx = o > k ? o : k, mn = o > k ? k : o;
+  return keep_max ? mx : mn;
+}
+
+// Sort one key per lane across the wave, descending: lane 0 receives the
+// largest (21 compare-exchange stages).
+__device__ __forceinline__ uint64_t wave_sort_desc(uint64_t k) {
+  const int lane = (int)(threadIdx.x & 63);
+  k = bitonic_stage<2, 1>(k, lane);
+  k = bitonic_stage<4, 2>(k, lane);
+  k = bitonic_stage<4, 1>(k, lane);
+  k = bitonic_stage<8, 4>(k, lane);
+  k = bitonic_stage<8, 2>(k, lane);
+  k = bitonic_stage<8, 1>(k, lane);
+  k = bitonic_stage<16, 8>(k, lane);
+  k = bitonic_stage<16, 4>(k, lane);
+  k = bitonic_stage<16, 2>(k, lane);
+  k = bitonic_stage<16, 1>(k, lane);
+  k = bitonic_stage<32, 16>(k, lane);
+  k = bitonic_stage<32, 8>(k, lane);
+  k = bitonic_stage<32, 4>(k, lane);
+  k = bitonic_stage<32, 2>(k, lane);
+  k = bitonic_stage<32, 1>(k, lane);
+  k = bitonic_stage<64, 32>(k, lane);
+  k = bitonic_stage<64, 16>(k, lane);
+  k = bitonic_stage<64, 8>(k, lane);
+  k = bitonic_stage<64, 4>(k, lane);
+  k = bitonic_stage<64, 2>(k, lane);
+  k = bitonic_stage<64, 1>(k, lane);
+  return k;
+}
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Append, in lane order, the values of the lanes with take set to a wave's
+// LDS list of capacity cap; count (the same in every lane) grows by their
+// number, also past cap (entries past cap are not written).
+template <typename T>
+__device__ __forceinline__ void wave_append(T* list, int& count, bool take, T v, int cap) {
+  const uint64_t bal = __ballot(take);
+  const int pos = count + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+  if (take && pos < cap) list[pos] = v;
+  count += __popcll(bal);
+}
+
 // Softmax statistics of the wave's union of disjoint sets: the maximum first,
 // then every lane's sums rescaled to it (T = sum e^(z-M) (z-M)) and added; the
 // argmax is the smallest id among lanes at the maximum.
@@ -342,12 +419,16 @@ __device__ void path_finish(const VocabArgs& a, int b, int n0, int n, int L, con
 
 }  // namespace
 
+constexpr int kMaxCandTiles = 256;  // >= K * (tile keys per thread)
+
 template <int KO>
 struct FinalizeLds {
   float st[4][4];
   uint64_t key[4][KO];
   float row[4];         // m, lse, -, argmax of the row (after the merge)
   uint64_t top[KO];     // the row's top-K keys
+  int ctile[4][kMaxCandTiles];  // per wave: candidate tiles
+  uint64_t surv[4][64];         // per wave: candidate logits that reach the threshold
   int par[kMaxNodes];
   int tok[kMaxNodes];
   uint8_t src[kMaxNodes];
@@ -415,7 +496,22 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
     const u32x4 pb = prow[t];
     st.merge(__uint_as_float(pb[0]), __uint_as_float(pb[1]), __uint_as_float(pb[2]), (int)pb[3]);
   }
-  sort_desc<LB>(tk);
+  // Candidate tiles of this wave.  H, the K-th largest of the lanes' largest
+  // tile keys, is the smallest of K distinct tile maxima, so the wave's K-th
+  // largest logit key is at least H: every entry of the row's top-K that lies
+  // in this wave's tiles has a key >= H and lies in a tile whose maximum key
+  // is >= H (at most K lanes hold such tiles).
+  uint64_t head = tk[0];
+#pragma unroll
+  for (int u = 1; u < LB; ++u) head = tk[u] > head ? tk[u] : head;
+  const uint64_t H = readlane64(wave_sort_desc(head), KO - 1);  // 0: fewer than K tiles
+  int* ct = sh.ctile[wave];
+  int nt = 0;
+#pragma unroll
+  for (int u = 0; u < LB; ++u) {
+    const uint32_t t = (uint32_t)key_id(tk[u]) / kLmTileRows;  // the tile of its maximum
+    wave_append(ct, nt, tk[u] != 0 && tk[u] >= H && t < (uint32_t)a.n_vtiles, (int)t, kMaxCandTiles);
+  }
   // the children of node li request their logit z_li[t] now (the parents have had time to arrive)
   bool is_child[NPT], tok_ok[NPT];
   float c_z[NPT];
@@ -426,31 +522,31 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
     tok_ok[u] = c_tok[u] >= 0 && c_tok[u] < a.vocab;
     c_z[u] = a.logits[(size_t)i * a.vocab + (is_child[u] && tok_ok[u] ? c_tok[u] : 0)];
   }
-  // The K largest tile keys of the wave.  Keys are distinct, so an entry of
-  // the row's top-K that lies in one of this wave's tiles lies in one of these
-  // K tiles (else K tile maxima of the wave would all exceed it).  The wave
-  // reads those tiles whole (64/K lanes per tile, K columns per lane) and takes
-  // their top-K; the row's top-K is the top-K of the waves' lists.
-  uint64_t top[KO];
-  wave_topk<LB, KO>(tk, top);
+  wave_lds_sync();
+  // The candidates' logits (8 tiles per pass: 8 lanes per tile, 8 columns
+  // each); those with a key >= H go to the wave's survivor list.
   const float* zrow = a.logits + (size_t)i * a.vocab;
-  uint64_t ck[KO];
+  uint64_t* sv = sh.surv[wave];
+  int nv = 0;
+  auto cand_pass = [&](int p0, uint64_t (&kz)[8]) {
+    const int c = p0 + (lane >> 3);
+    const int col0 = c < nt ? ct[c] * kLmTileRows + (lane & 7) : a.vocab;
+    float z[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) z[e] = col0 + 8 * e < a.vocab ? zrow[col0 + 8 * e] : 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint64_t kv = col0 + 8 * e < a.vocab ? make_key(z[e], col0 + 8 * e) : 0ull;
+      kz[e] = kv != 0 && kv >= H ? kv : 0ull;
+    }
+  };
   if (!spill) {
-    constexpr int LPT = 64 / KO;  // lanes per candidate tile
-    uint64_t mine = top[0];
+    for (int p0 = 0; p0 < nt; p0 += 8) {
+      uint64_t kz[8];
+      cand_pass(p0, kz);
 #pragma unroll
-    for (int k = 1; k < KO; ++k) mine = lane / LPT == k ? top[k] : mine;
-    const uint32_t tile = mine ? (uint32_t)key_id(mine) / kLmTileRows : 0xFFFFFFFFu;
-    const int col0 = tile < (uint32_t)a.n_vtiles ? (int)tile * kLmTileRows + lane % LPT : a.vocab;
-    float z[KO];
-#pragma unroll
-    for (int e = 0; e < KO; ++e) z[e] = col0 + LPT * e < a.vocab ? zrow[col0 + LPT * e] : 0.f;
-#pragma unroll
-    for (int e = 0; e < KO; ++e) ck[e] = col0 + LPT * e < a.vocab ? make_key(z[e], col0 + LPT * e) : 0ull;
-  } else {
-#pragma unroll
-    for (int k = 0; k < KO; ++k) ck[k] = 0ull;
-    for (int col = tid; col < a.vocab; col += NT) insert_desc<KO>(ck, make_key(zrow[col], col));
+      for (int e = 0; e < 8; ++e) wave_append(sv, nv, kz[e] != 0, kz[e], 64);
+    }
   }
   // the sequence's nodes go to LDS (the path reduction reads them)
   if (lay_ok) {
@@ -464,7 +560,7 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
       }
     }
   }
-  // the wave's statistics (by reductions) while the candidate logits arrive
+  // the wave's statistics (by reductions)
   wave_rowstats(st);
   if constexpr (WPR > 1) {
     if (lane == 0) {
@@ -474,18 +570,38 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
       sh.st[wave][3] = __int_as_float(st.am);
     }
   }
-  sort_desc<KO>(ck);
-  wave_topk<KO, KO>(ck, top);
-  if constexpr (WPR > 1) {
-    if (lane < KO) {
-      uint64_t mine = top[0];
+  wave_lds_sync();
+  // The wave's top-K: lane k < K receives the k-th key.  Normally at most 64
+  // survivors, sorted across the wave; otherwise (many equal values, or rows
+  // read whole) per-lane top-K lists and K rounds of wave maxima.
+  uint64_t kk;
+  if (!spill && nv <= 64) {
+    kk = wave_sort_desc(lane < nv ? sv[lane] : 0ull);
+  } else {
+    uint64_t ck[KO];
 #pragma unroll
-      for (int k = 1; k < KO; ++k) mine = lane == k ? top[k] : mine;
-      sh.key[wave][lane] = mine;
+    for (int k = 0; k < KO; ++k) ck[k] = 0ull;
+    if (!spill) {
+      for (int p0 = 0; p0 < nt; p0 += 8) {
+        uint64_t kz[8];
+        cand_pass(p0, kz);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) insert_desc<KO>(ck, kz[e]);
+      }
+    } else {
+      for (int col = tid; col < a.vocab; col += NT) insert_desc<KO>(ck, make_key(zrow[col], col));
     }
+    uint64_t top[KO];
+    wave_topk<KO, KO>(ck, top);
+    kk = 0ull;
+#pragma unroll
+    for (int k = 0; k < KO; ++k) kk = lane == k ? top[k] : kk;
+  }
+  if constexpr (WPR > 1) {
+    if (lane < KO) sh.key[wave][lane] = kk;
     __syncthreads();
     // across the waves (wave 0): lane w < WPR brings wave w's statistics, lane
-    // l < WPR*KO one key of wave l / KO's list
+    // l < WPR*K one key of wave l / K's list
     if (wave == 0) {
       const bool src_ok = lane < WPR;
       st.m = src_ok ? sh.st[lane][0] : -__builtin_huge_valf();
@@ -493,13 +609,9 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
       st.T = src_ok ? sh.st[lane][2] : 0.f;
       st.am = src_ok ? __float_as_int(sh.st[lane][3]) : 0x7FFFFFFF;
       wave_rowstats(st);
-      uint64_t k1[1] = {lane < WPR * KO ? sh.key[lane / KO][lane % KO] : 0ull};
-      wave_topk<1, KO>(k1, top);
+      kk = wave_sort_desc(lane < WPR * KO ? sh.key[lane / KO][lane % KO] : 0ull);
     }
   }
-  uint64_t key[KO];
-#pragma unroll
-  for (int k = 0; k < KO; ++k) key[k] = top[k];
   // row results: LDS for the predicates, memory for the outputs (wave 0)
   if (wave == 0) {
     const float logS = __logf(st.S);
@@ -508,19 +620,16 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
       sh.row[0] = st.m;
       sh.row[1] = lse;
       sh.row[3] = __int_as_float(st.am);
-#pragma unroll
-      for (int k = 0; k < KO; ++k) sh.top[k] = key[k];
       a.max_logit[i] = st.m;
       st_dev(a.argmax + i, st.am);
       a.lse[i] = lse;
       a.entropy[i] = logS - st.T / st.S;
     }
-#pragma unroll
-    for (int k = 0; k < KO; ++k)
-      if (lane == k && k < a.topk_out) {
-        a.topk_id[(size_t)i * a.topk_out + k] = key_id(key[k]);
-        a.topk_logprob[(size_t)i * a.topk_out + k] = key_value(key[k]) - lse;
-      }
+    if (lane < KO) sh.top[lane] = kk;
+    if (lane < a.topk_out) {
+      a.topk_id[(size_t)i * a.topk_out + lane] = key_id(kk);
+      a.topk_logprob[(size_t)i * a.topk_out + lane] = key_value(kk) - lse;
+    }
   }
   if constexpr (WPR > 1)
     __syncthreads();

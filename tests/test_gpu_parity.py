@@ -128,32 +128,41 @@ def test_edge_case_parity(rt, name):
 # (<= 64 tiles of 64 tokens), four waves with 2, 8 and 16 tile keys per thread,
 # and rows read whole (more than 4096 tiles).  "clustered" gives 24
 # consecutive tokens (across a tile boundary) near-copies of one LM-head row
-# scaled by 6-7.2, so that on many rows most of the top-k sits in one tile.
+# scaled by 6-7.2, so that on many rows most of the top-k sits in one tile;
+# "tied" gives 200 tokens one identical LM-head row (3x row 7) and token 5 the
+# row 3.5x row 7, so that on many rows the top-k is token 5 followed by equal
+# logits (more of them reach the candidate threshold than the sorted path takes).
 VOCAB_TIERS = [
-    (3000, 16, True),
-    (30000, 8, True),
-    (70000, 8, False),
-    (200000, 16, True),
-    (300000, 8, True),
+    (3000, 16, "clustered"),
+    (3000, 8, "tied"),
+    (30000, 8, "clustered"),
+    (30000, 16, "tied"),
+    (70000, 8, "plain"),
+    (200000, 16, "clustered"),
+    (300000, 8, "clustered"),
 ]
 
 
 @pytest.mark.timeout(300)
-@pytest.mark.parametrize("vocab,topk_out,clustered", VOCAB_TIERS)
-def test_vocab_tier_parity(rt, vocab, topk_out, clustered):
+@pytest.mark.parametrize("vocab,topk_out,mode", VOCAB_TIERS)
+def test_vocab_tier_parity(rt, vocab, topk_out, mode):
     parents = [[-1, 0, 1, 1, 3, 0], [-1, 0, 0, 2]]
     shp = synth.Shape("edge", "bf16", 4 * 64, 4, 1, 64, vocab, 2, 6, 8, topk_out)
     w = synth.custom(shp, parents, [70, 40], seed=211, poison_tail=True)
-    if clustered:
+    if mode != "plain":
         W = synth.bf16_bits_to_f32(w.lm_head).reshape(vocab, -1).copy()
-        c0 = 64 * 5 + 48
-        for k in range(24):
-            W[c0 + k] = W[7] * (6.0 + 0.05 * k) + 0.002 * W[100 + k]
+        if mode == "clustered":
+            c0 = 64 * 5 + 48
+            for k in range(24):
+                W[c0 + k] = W[7] * (6.0 + 0.05 * k) + 0.002 * W[100 + k]
+        else:
+            W[64:264] = W[7] * 3.0
+            W[5] = W[7] * 3.5
         w.lm_head = synth.f32_to_bf16_bits(W).reshape(w.lm_head.shape)
     w.params = synth.AcceptParams(topk=topk_out, tau=1.0, min_lookahead=1, max_relaxed=2)
-    _say(f"[vocab {vocab} k={topk_out} clustered={clustered}] building")
+    _say(f"[vocab {vocab} k={topk_out} {mode}] building")
     case = workload.finish(w)
-    _say(f"[vocab {vocab} k={topk_out} clustered={clustered}] running GPU step")
+    _say(f"[vocab {vocab} k={topk_out} {mode}] running GPU step")
     compare(case, rt.run(case.w), f"vocab {vocab}")
 
 
