@@ -273,11 +273,11 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
     lm.m_rows = a.total_nodes;
     lm.vocab = s.vocab;
     lm.hidden_size = s.hidden;
-    // token rows per workgroup 16*mb: up to 64 in the plain kernel, 96, 128 or 256 in
+    // token rows per workgroup 16*mb: up to 64 in the plain kernel, 128 or 256 in
     // the tiled one (bf16), so that W is streamed once for up to 256 rows
     const int M = a.total_nodes;
     int mb = M <= 16 ? 1 : M <= 32 ? 2 : M <= 48 ? 3 : 4;
-    if (M > 64 && s.dtype == RESPEC_BF16) mb = M <= 96 ? 6 : M <= 128 ? 8 : 16;
+    if (M > 64 && s.dtype == RESPEC_BF16) mb = M <= 128 ? 8 : 16;
     lm.n_mtiles = cdiv(M, 16 * mb);
     lm.partials = full ? reinterpret_cast<float*>(ws + plan->off_part) : nullptr;
     lm.n_vtiles = plan->n_vtiles;

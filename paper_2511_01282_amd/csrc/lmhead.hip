@@ -364,191 +364,204 @@ __global__ __launch_bounds__(256, 2) void lmhead_persistent_kernel(LmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Tiled variant for many token rows (up to 256 per pass).  With many token
-// rows the x tile, not W, dominates what a workgroup pulls through its CU, so
-// a workgroup here owns 128 vocabulary rows (each x row it loads serves twice
-// as many W rows):
-//   - 4 waves in a 2 x 2 grid: wave (wv, wm) computes vocabulary rows
-//     64*wv .. +63 (four 16-row blocks, one statistics tile) against token rows
-//     16*MB*wm .. +16*MB-1;
-//   - K advances in 128-byte steps.  The W fragments and this thread's share
-//     of the x tile of step c+3 are requested together, right after step c's
-//     matrix products, so waiting for the oldest step (W and x of step c)
-//     never waits for the newer loads: steps c+1 and c+2 stay in flight.  x
-//     goes from registers to a double-buffered LDS tile (one barrier per
-//     step), from which every wave reads its B fragments;
-//   - each wave reduces its own 64 vocabulary rows to the per-tile statistics.
+// Tiled variant for many token rows (65 to 256 per pass, bf16).  With many
+// token rows the x rows, not W, dominate what a workgroup pulls through its
+// CU, so a workgroup owns 128 vocabulary rows (two statistics tiles), and
+// every byte of W and x it needs crosses the CU once per pass:
+//   - the 128 W rows of a K step go through a double-buffered LDS tile
+//     (requested into registers, 4 pieces of 16 bytes per thread, written to
+//     LDS; one barrier per step), from which every wave reads its A
+//     fragments;
+//   - wave w owns token rows 16*TB*w .. +16*TB-1 and requests its x fragments
+//     (the B operands) straight into registers; token blocks past the last
+//     row are not multiplied;
+//   - K advances in 128-byte steps through a ring of four register stages:
+//     step c is consumed while steps c+1 .. c+3 are in flight, and step c+4
+//     is requested into the freed registers right after step c's products;
+//   - each wave reduces its token rows over each 64-row half of the tile to
+//     the per-tile statistics.
 constexpr int kTlStep = 128;                 // bytes of a row per K step
 constexpr int kTlPieces = kTlStep / 64;      // mma_k64 calls per K step
-constexpr int kTlXStride = kTlStep + 16;     // LDS row stride of the x tile
+constexpr int kTlWStride = kTlStep + 16;     // LDS row stride of the W tile
 constexpr int kTlRows = 128;                 // vocabulary rows per workgroup
+constexpr int kTlRing = 4;                   // register stages
 
-template <int MB>
+template <int TB>
 __device__ __forceinline__ void lmhead_tiled_body(const LmArgs& a) {
-  constexpr int VB = 4;                            // 16-row vocabulary blocks per wave
-  constexpr int MT = 32 * MB;                      // token rows per workgroup
-  constexpr int XP = MT * kTlStep / 16 / 256;      // 16-byte x pieces per thread per step
-  __shared__ __align__(16) unsigned char sx[2 * MT * kTlXStride];
+  constexpr int VB = kTlRows / 16;                  // 16-row vocabulary blocks (all waves)
+  constexpr int MT = 64 * TB;                       // token rows per workgroup
+  constexpr int WP = kTlRows * kTlStep / 16 / 256;  // 16-byte W pieces per thread per step
+  __shared__ __align__(16) unsigned char sw[2 * kTlRows * kTlWStride];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int wv = wave & 1, wm = wave >> 1;
   const int n_mt = a.n_mtiles;
   const int id = blockIdx.x;
   const int grp = id / (8 * n_mt), rem = id % (8 * n_mt);
   const int vt = grp * 8 + rem % 8, mt = rem / 8;  // vt: 128-row tile
   if (vt * kTlRows >= a.vocab) return;
-  const int v0 = vt * kTlRows + 64 * wv;           // first vocabulary row of this wave
-  const int stat_tile = 2 * vt + wv;               // this wave's 64-row statistics tile
-  const int m0 = mt * MT;                          // first token row of the workgroup
+  const int v0 = vt * kTlRows;                     // first vocabulary row of the workgroup
+  const int m0 = mt * MT + 16 * TB * wave;         // first token row of this wave
+  // (uniform per wave) token blocks of this wave that hold a row
+  const int tbl = __builtin_amdgcn_readfirstlane(min(TB, max(0, (a.m_rows - m0 + 15) / 16)));
   const size_t row_bytes = (size_t)a.hidden_size * 2;
   const int n_steps = (int)(row_bytes / kTlStep);  // >= 4 (hidden*2 is a multiple of 512)
   const int rot = vt % n_steps;                    // per-workgroup K start (spreads the channels)
   auto step_of = [&](int c) { return c + rot < n_steps ? c + rot : c + rot - n_steps; };
 
-  const char* wrow[VB];
+  const char* wpiece[WP];
 #pragma unroll
-  for (int vb = 0; vb < VB; ++vb) {
-    const int v = min(v0 + 16 * vb + lr, a.vocab - 1);  // rows past V: a valid row, results not stored
-    wrow[vb] = reinterpret_cast<const char*>(a.w) + (size_t)v * row_bytes + lg * 16;
+  for (int q = 0; q < WP; ++q) {
+    const int pidx = threadIdx.x + 256 * q;
+    const int r = pidx / (kTlStep / 16), pc = pidx % (kTlStep / 16);
+    const int v = min(v0 + r, a.vocab - 1);  // rows past V: a valid row, results not stored
+    wpiece[q] = reinterpret_cast<const char*>(a.w) + (size_t)v * row_bytes + pc * 16;
   }
-  const char* xbase = reinterpret_cast<const char*>(a.x);
+  const char* xrow[TB];
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb) {
+    const int m = min(m0 + 16 * tb + lr, a.m_rows - 1);  // rows past M: a valid row, results not stored
+    xrow[tb] = reinterpret_cast<const char*>(a.x) + (size_t)m * row_bytes + lg * 16;
+  }
 
   struct Stage {
-    u32x4 w[VB][kTlPieces];
-    u32x4 x[XP];
+    u32x4 w[WP];
+    u32x4 x[TB][kTlPieces];
   };
   auto issue = [&](Stage& st, int c) {
     const size_t off = (size_t)step_of(c) * kTlStep;
 #pragma unroll
-    for (int vb = 0; vb < VB; ++vb)
+    for (int q = 0; q < WP; ++q) st.w[q] = ld16(wpiece[q] + off);
+    // (every block is requested, so that each stage holds the same count of
+    // requests; a block past the last row reads row M-1 in every lane, one
+    // cache line per request)
 #pragma unroll
-      for (int kp = 0; kp < kTlPieces; ++kp) st.w[vb][kp] = ld16(wrow[vb] + off + kp * 64);
+    for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-    for (int t = 0; t < XP; ++t) {
-      const int idx = threadIdx.x + 256 * t;
-      const int r = idx / (kTlStep / 16), pc = idx % (kTlStep / 16);
-      const int m = min(m0 + r, a.m_rows - 1);  // rows past M: a valid row, results not stored
-      st.x[t] = ld16(xbase + (size_t)m * row_bytes + off + pc * 16);
-    }
+      for (int kp = 0; kp < kTlPieces; ++kp) st.x[tb][kp] = ld16(xrow[tb] + off + kp * 64);
   };
-  auto stage_x = [&](const Stage& st, unsigned char* buf) {
+  auto stage_w = [&](const Stage& st, unsigned char* buf) {
 #pragma unroll
-    for (int t = 0; t < XP; ++t) {
-      const int idx = threadIdx.x + 256 * t;
-      const int r = idx / (kTlStep / 16), pc = idx % (kTlStep / 16);
-      *reinterpret_cast<u32x4*>(buf + r * kTlXStride + pc * 16) = st.x[t];
+    for (int q = 0; q < WP; ++q) {
+      const int pidx = threadIdx.x + 256 * q;
+      const int r = pidx / (kTlStep / 16), pc = pidx % (kTlStep / 16);
+      *reinterpret_cast<u32x4*>(buf + r * kTlWStride + pc * 16) = st.w[q];
     }
   };
 
-  f32x4 acc[VB][MB];
+  f32x4 acc[VB][TB];
 #pragma unroll
   for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) acc[vb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int tb = 0; tb < TB; ++tb) acc[vb][tb] = f32x4{0.f, 0.f, 0.f, 0.f};
   auto mma_step = [&](const Stage& st, const unsigned char* buf) {
 #pragma unroll
     for (int kp = 0; kp < kTlPieces; ++kp) {
-      u32x4 xb[MB];
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-        xb[mb] = *reinterpret_cast<const u32x4*>(buf + (MB * 16 * wm + 16 * mb + lr) * kTlXStride + kp * 64 + lg * 16);
+      u32x4 wf[VB];
 #pragma unroll
       for (int vb = 0; vb < VB; ++vb)
+        wf[vb] = *reinterpret_cast<const u32x4*>(buf + (16 * vb + lr) * kTlWStride + kp * 64 + lg * 16);
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) acc[vb][mb] = mma_k64(bf16_t{}, st.w[vb][kp], xb[mb], acc[vb][mb]);
+      for (int tb = 0; tb < TB; ++tb)
+        if (tb < tbl)
+#pragma unroll
+          for (int vb = 0; vb < VB; ++vb) acc[vb][tb] = mma_k64(bf16_t{}, wf[vb], st.x[tb][kp], acc[vb][tb]);
     }
   };
 
-  // three stages in a ring: step c is consumed while steps c+1 and c+2 are in
-  // flight; after its products step c+3 goes into the freed registers.  The
-  // steady-state loop only refills real steps (the same count of requests
+  // The steady-state loop only refills real steps (the same count of requests
   // behind every step on every pass); the last steps (straight-line code)
-  // refill while steps remain, so nothing is in flight at the epilogue.  x
+  // refill while steps remain, so nothing is in flight at the epilogue.  W
   // alternates between two LDS buffers (the barrier of step c+1 orders step
   // c's reads before the writes of step c+2).
-  Stage ring[3];
+  Stage ring[kTlRing];
 #pragma unroll
-  for (int j = 0; j < 3; ++j) {
+  for (int j = 0; j < kTlRing; ++j) {
     issue(ring[j], min(j, n_steps - 1));
     __builtin_amdgcn_sched_barrier(0);
   }
   auto step = [&](Stage& st, int c, bool refill) {
-    unsigned char* buf = sx + (c & 1) * MT * kTlXStride;
-    stage_x(st, buf);
+    unsigned char* buf = sw + (c & 1) * kTlRows * kTlWStride;
+    stage_w(st, buf);
     __syncthreads();
     mma_step(st, buf);
-    if (refill) issue(st, c + 3);
+    if (refill) issue(st, c + kTlRing);
     __builtin_amdgcn_sched_barrier(0);  // keep the requests here, ahead of the next step's wait
   };
   int c = 0;
-  for (; c + 6 <= n_steps; c += 3) {
-    step(ring[0], c, true);
-    step(ring[1], c + 1, true);
-    step(ring[2], c + 2, true);
+  for (; c + 2 * kTlRing <= n_steps; c += kTlRing) {
+#pragma unroll
+    for (int j = 0; j < kTlRing; ++j) step(ring[j], c + j, true);
   }
 #pragma unroll
-  for (int j = 0; j < 5; ++j)
-    if (c + j < n_steps) step(ring[j % 3], c + j, c + j + 3 < n_steps);
+  for (int j = 0; j < 2 * kTlRing - 1; ++j)
+    if (c + j < n_steps) step(ring[j % kTlRing], c + j, c + j + kTlRing < n_steps);
 
-  // logits: lane holds z[m0 + 16*MB*wm + 16*mb + lr][v0 + 16*vb + 4*lg + i]
+  // logits: lane holds z[m0 + 16*tb + lr][v0 + 16*vb + 4*lg + i]
   const bool vec_ok = (a.vocab & 3) == 0;
 #pragma unroll
-  for (int vb = 0; vb < VB; ++vb)
+  for (int tb = 0; tb < TB; ++tb) {
+    const int m = m0 + 16 * tb + lr;
+    if (tb >= tbl || m >= a.m_rows) continue;
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const int m = m0 + MB * 16 * wm + 16 * mb + lr;
+    for (int vb = 0; vb < VB; ++vb) {
       const int vv = v0 + 16 * vb + 4 * lg;
-      if (m >= a.m_rows) continue;
       float* dst = a.logits + (size_t)m * a.vocab + vv;
       if (vec_ok && vv + 3 < a.vocab) {
-        *reinterpret_cast<f32x4*>(dst) = acc[vb][mb];
+        *reinterpret_cast<f32x4*>(dst) = acc[vb][tb];
       } else {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          if (vv + i < a.vocab) dst[i] = acc[vb][mb][i];
+          if (vv + i < a.vocab) dst[i] = acc[vb][tb][i];
       }
     }
-  if (!a.partials || v0 >= a.vocab) return;  // (a wave past V has no statistics tile)
+  }
+  if (!a.partials) return;
 
-  // per-tile statistics of each token row over this wave's 64 logits
+  // per-tile statistics of each token row over each 64-row half of the tile
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    float mx = kNegInf;
+  for (int half = 0; half < 2; ++half) {
+    const int vh = v0 + 64 * half;
+    if (vh >= a.vocab) break;  // (no statistics tile past V)
 #pragma unroll
-    for (int vb = 0; vb < VB; ++vb)
+    for (int tb = 0; tb < TB; ++tb) {
+      if (tb >= tbl) continue;
+      float mx = kNegInf;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int col = v0 + 16 * vb + 4 * lg + i;
-        mx = col < a.vocab ? fmaxf(mx, acc[vb][mb][i]) : mx;
-      }
-    RowStats st;
-    st.init();
-    st.m = mx;
+      for (int vb = 4 * half; vb < 4 * half + 4; ++vb)
 #pragma unroll
-    for (int vb = 0; vb < VB; ++vb)
+        for (int i = 0; i < 4; ++i) {
+          const int col = v0 + 16 * vb + 4 * lg + i;
+          mx = col < a.vocab ? fmaxf(mx, acc[vb][tb][i]) : mx;
+        }
+      RowStats st;
+      st.init();
+      st.m = mx;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int col = v0 + 16 * vb + 4 * lg + i;
-        const bool ok = col < a.vocab;
-        const float d = acc[vb][mb][i] - mx;
-        const float e = ok ? __expf(d) : 0.f;
-        st.S += e;
-        st.T += ok ? e * d : 0.f;
-        st.am = (ok && acc[vb][mb][i] == mx) ? min(st.am, col) : st.am;
-      }
-    st.merge_level<4>();  // lane groups of a token row: xor 16, xor 32
-    st.merge_level<5>();
-    const int m = m0 + MB * 16 * wm + 16 * mb + lr;
-    if (lg == 0 && m < a.m_rows)
-      *reinterpret_cast<u32x4*>(a.partials + ((size_t)m * a.n_vtiles + stat_tile) * kTileWords) =
-          u32x4{__float_as_uint(st.m), __float_as_uint(st.S), __float_as_uint(st.T), (uint32_t)st.am};
+      for (int vb = 4 * half; vb < 4 * half + 4; ++vb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int col = v0 + 16 * vb + 4 * lg + i;
+          const bool ok = col < a.vocab;
+          const float d = acc[vb][tb][i] - mx;
+          const float e = ok ? __expf(d) : 0.f;
+          st.S += e;
+          st.T += ok ? e * d : 0.f;
+          st.am = (ok && acc[vb][tb][i] == mx) ? min(st.am, col) : st.am;
+        }
+      st.merge_level<4>();  // lane groups of a token row: xor 16, xor 32
+      st.merge_level<5>();
+      const int m = m0 + 16 * tb + lr;
+      if (lg == 0 && m < a.m_rows)
+        *reinterpret_cast<u32x4*>(a.partials + ((size_t)m * a.n_vtiles + 2 * vt + half) * kTileWords) =
+            u32x4{__float_as_uint(st.m), __float_as_uint(st.S), __float_as_uint(st.T), (uint32_t)st.am};
+    }
   }
 }
 
-template <int MB>
+template <int TB>
 __global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
-  lmhead_tiled_body<MB>(a);
+  lmhead_tiled_body<TB>(a);
 }
 
 // Workgroups of a kernel that fit on the device at once (host occupancy
@@ -596,15 +609,13 @@ hipError_t launch_lmhead(int dtype, int mb, const LmArgs& a, hipStream_t s, hipE
   const int n_vt = (a.vocab + kLmRows - 1) / kLmRows;
   const int n_grp = (n_vt + 7) / 8;
   dim3 grid(n_grp * 8 * a.n_mtiles);
-  if (mb == 6 || mb == 8 || mb == 16) {  // tiled variant: MT = 96, 128 or 256 token rows, 128-row vocabulary tiles (bf16)
+  if (mb == 8 || mb == 16) {  // tiled variant: MT = 128 or 256 token rows, 128-row vocabulary tiles (bf16)
     if (dtype != 1) return hipErrorInvalidValue;
     const int n_vt2 = (a.vocab + kTlRows - 1) / kTlRows;
     dim3 tgrid(((n_vt2 + 7) / 8) * 8 * a.n_mtiles);
     const dim3 blk(256);
-    const int tmb = mb / 2;
-    return tmb == 3   ? launch_k(lmhead_tiled_kernel<3>, tgrid, blk, 0, s, nullptr, ev_stop, a)
-           : tmb == 4 ? launch_k(lmhead_tiled_kernel<4>, tgrid, blk, 0, s, nullptr, ev_stop, a)
-                      : launch_k(lmhead_tiled_kernel<8>, tgrid, blk, 0, s, nullptr, ev_stop, a);
+    return mb == 8 ? launch_k(lmhead_tiled_kernel<2>, tgrid, blk, 0, s, nullptr, ev_stop, a)
+                   : launch_k(lmhead_tiled_kernel<4>, tgrid, blk, 0, s, nullptr, ev_stop, a);
   }
   return dtype == 1 ? launch_mb<bf16_t>(mb, grid, a, s, ev_stop) : launch_mb<float>(mb, grid, a, s, ev_stop);
 }
