@@ -21,6 +21,7 @@ struct respec_verify_plan {
   int nb, wr, wk, rows_per_wg, n_rowblk, attn_threads, nsplit_cap;
   int attn_shared;        // bf16 with several waves of rows per KV head: KV tiles shared through LDS
   int attn_stages;        // ring slots of the shared-tile kernel
+  int attn_kg;            // key groups of the shared-tile kernel
   int attn_wg_target;     // workgroups the splits aim for
   size_t attn_lds;
   // vocabulary statistics: tiles of the LM head and top-K list length
@@ -108,17 +109,19 @@ respec_status respec_verify_create(const respec_verify_shape* shape, respec_veri
   p->nb = nb;
   p->attn_shared = es == 2 && rg >= 2;
   if (p->attn_shared) {
-    // up to 8 waves of rows read every KV tile once, from a shared LDS ring; a
-    // workgroup of more than 4 such waves fills a CU (two waves per SIMD)
+    // up to 8 waves of rows read every KV tile once, from a shared 8-slot LDS
+    // ring, one workgroup per CU; up to 4 waves of rows, a second key group of
+    // as many waves takes every other tile (one workgroup fills the CU, and
+    // its two halves stay in step)
     p->wr = rg < 8 ? rg : 8;
     p->n_rowblk = cdiv(rg, p->wr);
     p->wk = 1;
+    p->attn_kg = p->wr <= 4 ? 2 : 1;
     p->rows_per_wg = p->wr * rb;
-    p->attn_threads = 64 * p->wr;
-    // two workgroups per CU up to 4 waves (5-slot rings), else one (8 slots)
-    p->attn_stages = p->wr <= 4 ? 5 : 8;
+    p->attn_threads = 64 * p->wr * p->attn_kg;
+    p->attn_stages = 8;
     p->attn_lds = (size_t)shared_ring_bytes(s.head_dim, p->attn_stages);
-    p->attn_wg_target = kCUs * (p->wr <= 4 ? 2 : 1);
+    p->attn_wg_target = kCUs;
   } else {
     p->wr = rg < 4 ? rg : 4;
     p->n_rowblk = cdiv(rg, p->wr);
@@ -216,7 +219,7 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   int32_t* cnt = reinterpret_cast<int32_t*>(ws + plan->off_cnt);
 
   if (!plan->lds_ready.load(std::memory_order_acquire)) {
-    const hipError_t e = plan->attn_shared ? set_tree_attn_shared_lds_limit(s.head_dim, plan->attn_stages, plan->attn_lds)
+    const hipError_t e = plan->attn_shared ? set_tree_attn_shared_lds_limit(s.head_dim, plan->attn_stages, plan->attn_kg, plan->attn_lds)
                                            : set_tree_attn_lds_limit(s.dtype, s.head_dim, plan->nb, plan->attn_lds);
     if (e != hipSuccess) return RESPEC_ERR_HIP;
     plan->lds_ready.store(true, std::memory_order_release);
@@ -254,7 +257,7 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   dim3 agrid(at.nsplit, s.n_kv_heads * plan->n_rowblk, a.batch);
   const hipError_t ae =
       plan->attn_shared
-          ? launch_tree_attn_shared(s.head_dim, plan->nb, plan->attn_stages, agrid, plan->attn_threads,
+          ? launch_tree_attn_shared(s.head_dim, plan->nb, plan->attn_stages, plan->attn_kg, agrid, plan->attn_threads,
                                     plan->attn_lds, at, st, ev ? ev[0] : nullptr)
           : launch_tree_attn(s.dtype, s.head_dim, plan->nb, agrid, plan->attn_threads, plan->attn_lds, at, st,
                              ev ? ev[0] : nullptr);

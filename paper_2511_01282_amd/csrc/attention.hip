@@ -757,7 +757,7 @@ __device__ __forceinline__ void dma_half_asm(uint32_t lds_dst, const char* base,
   }
 }
 
-template <int D, int NB, int S>
+template <int D, int NB, int S, int KG>
 __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
   constexpr int KCH = D * 2 / 64;
   constexpr int DB = D / 16;
@@ -765,13 +765,15 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
   constexpr int kTile = kKvTile * D * 2;  // bytes of one K or V half-tile
   constexpr int kStage = 2 * kTile;
   constexpr int kLpt = kTile / 1024;      // DMA instructions per half-tile
-  static_assert(S >= 3 && (S - 2) * kLpt <= 63, "vmcnt holds at most 63 pending requests");
+  static_assert(S >= 2 * KG + 1 && (S - 2 * KG) * kLpt <= 63, "vmcnt holds at most 63 pending requests");
 
   extern __shared__ __align__(16) unsigned char smem[];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)smem;
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int grp = KG > 1 ? __builtin_amdgcn_readfirstlane(wave / a.wr) : 0;  // key group
+  const int rw = wave - grp * a.wr;                                            // row wave
   const int lr = lane & 15, lg = lane >> 4;
   const int b = blockIdx.z;
   const int g = blockIdx.y / a.n_rowblk, rb = blockIdx.y % a.n_rowblk;
@@ -798,7 +800,7 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
 
   int p_lo = a.parent[node0 + min(lane, n_nodes - 1)];
   int p_hi = a.parent[node0 + min(lane + 64, n_nodes - 1)];
-  const int row_wave = row_wg + wave * RB;
+  const int row_wave = row_wg + rw * RB;
   u32x4 qf[NB][KCH];
   int qnode[NB];
 #pragma unroll
@@ -827,10 +829,10 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
   for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
     for (int kc = 0; kc < KCH; ++kc) asm volatile("" : "+v"(qf[nb][kc]));
-  // the first S - 1 tiles (kv_hi >= 1, so every clamped row is a valid cache row)
+  // the first S - KG tiles (kv_hi >= 1, so every clamped row is a valid cache row)
   if (wave < 2) {
 #pragma unroll
-    for (int st = 0; st < S - 1; ++st) {
+    for (int st = 0; st < S - KG; ++st) {
       if (wave == 0)
         dma_half_asm<D, false>(lds0 + st * kStage, kbase, tile_row(st), kv_hi, lane);
       else
@@ -855,47 +857,64 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
   // row blocks of this wave that hold a live row (blocks past the group's last row are skipped)
   const int nbc = __builtin_amdgcn_readfirstlane(min(NB, max(0, (R - row_wave + 15) / 16)));
 
-  int slot = 0;  // ring slot of tile i
-  for (int i = 0; i < n_tiles; ++i) {
-    const int refill = slot == 0 ? S - 1 : slot - 1;  // slot of tile i-1, refilled with tile i+S-1
-    // tile i has landed (a requesting wave waits for its own requests) and every
-    // wave's reads of tile i-1 are done: one barrier covers both
+  // Pass j consumes tiles KG*j .. KG*j+KG-1 (group q takes tile KG*j+q) from
+  // slots s0 .. s0+KG-1 (mod S); the slots of the previous pass's tiles are
+  // refilled with the tiles S ahead of them.
+  int s0 = 0;  // ring slot of tile KG*j
+  for (int j = 0; KG * j < n_tiles; ++j) {
+    // tiles KG*j .. KG*j+KG-1 have landed (a requesting wave waits for its own
+    // requests) and every wave's reads of the previous pass are done: one
+    // barrier covers both
     if (wave < 2)
-      asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"((S - 2) * kLpt) : "memory");
+      asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"((S - 2 * KG) * kLpt) : "memory");
     else
       asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    if (wave == 0)
-      dma_half_asm<D, false>(lds0 + refill * kStage, kbase, tile_row(i + S - 1), kv_hi, lane);
-    else if (wave == 1)
-      dma_half_asm<D, true>(lds0 + refill * kStage + kTile, vbase, tile_row(i + S - 1), kv_hi, lane);
-    const unsigned char* kt = smem + slot * kStage;
-    KTile<D> kf;
-    {
-      const int sw = kswz<D>(lr);  // kswz(16 + lr) == kswz(lr)
+    if (wave < 2) {
+#pragma unroll
+      for (int q = 0; q < KG; ++q) {
+        int sl = s0 - KG + q;
+        sl = sl < 0 ? sl + S : sl;
+        const int t_new = KG * j - KG + q + S;
+        if (wave == 0)
+          dma_half_asm<D, false>(lds0 + sl * kStage, kbase, tile_row(t_new), kv_hi, lane);
+        else
+          dma_half_asm<D, true>(lds0 + sl * kStage + kTile, vbase, tile_row(t_new), kv_hi, lane);
+      }
+    }
+    const int t = KG * j + grp;
+    if (t < n_tiles) {
+      int slot = s0 + grp;
+      slot = slot >= S ? slot - S : slot;
+      const unsigned char* kt = smem + slot * kStage;
+      KTile<D> kf;
+      {
+        const int sw = kswz<D>(lr);  // kswz(16 + lr) == kswz(lr)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int kc = 0; kc < KCH; ++kc)
+            kf.k[kb][kc] = *reinterpret_cast<const u32x4*>(kt + (16 * kb + lr) * D * 2 + (((4 * kc + lg) ^ sw) << 4));
+      }
+      f32x4 s[2][NB];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int kc = 0; kc < KCH; ++kc)
-          kf.k[kb][kc] = *reinterpret_cast<const u32x4*>(kt + (16 * kb + lr) * D * 2 + (((4 * kc + lg) ^ sw) << 4));
+        for (int nb = 0; nb < NB; ++nb) {
+          if (nb >= nbc) break;
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int kc = 0; kc < KCH; ++kc) acc = mma_k64(bf16_t{}, kf.k[kb][kc], qf[nb][kc], acc);
+          s[kb][nb] = acc;
+        }
+      u32x4 vf[DB];
+      read_vt_bf16<D>(kt + kTile, lane, vf);
+      u32x4 phi[NB], plo[NB];
+      softmax_p_bf16<D, NB>(s, kv_lo + t * kKvTile, kv_hi, L, qnode, anc, a.scale_log2, m_run, l_run, o, lane, phi,
+                            plo, nbc);
+      pv_bf16<D, NB, DB>(vf, 0, phi, plo, o, nbc);
     }
-    f32x4 s[2][NB];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        if (nb >= nbc) break;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kc = 0; kc < KCH; ++kc) acc = mma_k64(bf16_t{}, kf.k[kb][kc], qf[nb][kc], acc);
-        s[kb][nb] = acc;
-      }
-    u32x4 vf[DB];
-    read_vt_bf16<D>(kt + kTile, lane, vf);
-    u32x4 phi[NB], plo[NB];
-    softmax_p_bf16<D, NB>(s, kv_lo + i * kKvTile, kv_hi, L, qnode, anc, a.scale_log2, m_run, l_run, o, lane, phi,
-                          plo, nbc);
-    pv_bf16<D, NB, DB>(vf, 0, phi, plo, o, nbc);
-    slot = slot == S - 1 ? 0 : slot + 1;
+    s0 += KG;
+    s0 = s0 >= S ? s0 - S : s0;
   }
   // the DMAs past the last tile must land before the workgroup's LDS is released
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -905,11 +924,45 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
     l_run[nb] += xchg<4>(l_run[nb]);
     l_run[nb] += xchg<5>(l_run[nb]);
   }
+  if constexpr (KG > 1) {
+    // Key group 1 hands its (max, sum, O) to group 0 through the ring's LDS,
+    // lane by lane (both hold the same rows in the same lanes):
+    //   M = max(m0, m1),  w_q = 2^(m_q - M),  l = w0 l0 + w1 l1,  O = w0 O0 + w1 O1.
+    constexpr int kX = DB * NB * 4 + 2 * NB;  // floats per lane
+    __syncthreads();  // every wave is done with the ring
+    float* xo = reinterpret_cast<float*>(smem) + (size_t)rw * kX * 64 + lane;
+    if (grp == 1) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) xo[((nb * DB + db) * 4 + i) * 64] = o[db][nb][i];
+        xo[(DB * NB * 4 + 2 * nb) * 64] = m_run[nb];
+        xo[(DB * NB * 4 + 2 * nb + 1) * 64] = l_run[nb];
+      }
+    }
+    __syncthreads();
+    if (grp != 0) return;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const float m1 = xo[(DB * NB * 4 + 2 * nb) * 64], l1 = xo[(DB * NB * 4 + 2 * nb + 1) * 64];
+      const float M = fmaxf(m_run[nb], m1);
+      const float w0 = m_run[nb] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m_run[nb] - M);
+      const float w1 = m1 == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
+      l_run[nb] = l_run[nb] * w0 + l1 * w1;
+      m_run[nb] = M;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[db][nb][i] = o[db][nb][i] * w0 + xo[((nb * DB + db) * 4 + i) * 64] * w1;
+    }
+  }
   const int bgr = (b * a.n_kv_heads + g) * a.n_rowblk + rb;
   const size_t pbase = ((size_t)bgr * a.nsplit + split) * a.rows_per_wg;
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    const int rl = wave * RB + 16 * nb + lr;
+    const int rl = rw * RB + 16 * nb + lr;
     if (row_wg + rl >= R) continue;  // rows past the group's last are never merged
 #pragma unroll
     for (int db = 0; db < DB; ++db)
@@ -1021,32 +1074,31 @@ hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int thre
 }
 
 template <int D>
-static hipError_t shared_ring(int stages, bool launch, dim3 grid, int threads, size_t lds, const AttnArgs& a,
+static hipError_t shared_ring(int stages, int kg, bool launch, dim3 grid, int threads, size_t lds, const AttnArgs& a,
                               hipStream_t s, hipEvent_t ev_start) {
   const void* f = nullptr;
-  switch (stages) {
-    case 5: f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, 5>); break;
-    case 8: f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, 8>); break;
-    default: return hipErrorInvalidValue;
-  }
+  if (stages == 8 && kg == 1) f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, 8, 1>);
+  if (stages == 8 && kg == 2) f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, 8, 2>);
+  if (!f) return hipErrorInvalidValue;
   if (!launch) return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (stages == 5) return launch_k(tree_attn_shared_kernel<D, 2, 5>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
-  return launch_k(tree_attn_shared_kernel<D, 2, 8>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
+  if (kg == 1) return launch_k(tree_attn_shared_kernel<D, 2, 8, 1>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
+  return launch_k(tree_attn_shared_kernel<D, 2, 8, 2>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
 }
 
-hipError_t launch_tree_attn_shared(int head_dim, int nb, int stages, dim3 grid, int threads, size_t lds,
+hipError_t launch_tree_attn_shared(int head_dim, int nb, int stages, int kg, dim3 grid, int threads, size_t lds,
                                    const AttnArgs& a, hipStream_t s, hipEvent_t ev_start) {
-  if (nb != 2 || threads < 128 || threads > 512 || threads % 64) return hipErrorInvalidValue;  // 2..8 waves
+  if (nb != 2 || threads < 128 || threads > 512 || threads % 64 || threads != 64 * a.wr * kg)
+    return hipErrorInvalidValue;  // 2..8 waves
   if (lds < (size_t)shared_ring_bytes(head_dim, stages)) return hipErrorInvalidValue;
-  if (head_dim == 128) return shared_ring<128>(stages, true, grid, threads, lds, a, s, ev_start);
-  if (head_dim == 64) return shared_ring<64>(stages, true, grid, threads, lds, a, s, ev_start);
+  if (head_dim == 128) return shared_ring<128>(stages, kg, true, grid, threads, lds, a, s, ev_start);
+  if (head_dim == 64) return shared_ring<64>(stages, kg, true, grid, threads, lds, a, s, ev_start);
   return hipErrorInvalidValue;
 }
 
-hipError_t set_tree_attn_shared_lds_limit(int head_dim, int stages, size_t lds) {
+hipError_t set_tree_attn_shared_lds_limit(int head_dim, int stages, int kg, size_t lds) {
   const AttnArgs none{};
-  if (head_dim == 128) return shared_ring<128>(stages, false, dim3(), 0, lds, none, nullptr, nullptr);
-  if (head_dim == 64) return shared_ring<64>(stages, false, dim3(), 0, lds, none, nullptr, nullptr);
+  if (head_dim == 128) return shared_ring<128>(stages, kg, false, dim3(), 0, lds, none, nullptr, nullptr);
+  if (head_dim == 64) return shared_ring<64>(stages, kg, false, dim3(), 0, lds, none, nullptr, nullptr);
   return hipErrorInvalidValue;
 }
 

@@ -80,11 +80,12 @@ hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int thre
 hipError_t set_tree_attn_lds_limit(int dtype, int head_dim, int nb, size_t lds);
 hipError_t launch_attn_merge(int dtype, int head_dim, dim3 grid, const AttnArgs& a, hipStream_t s,
                              hipEvent_t ev_stop = nullptr);
-// bf16 only; 2-8 waves, each owning 32 query rows (nb = 2); KV tiles shared
-// through an LDS ring of `stages` (5 or 8) K+V tiles
-hipError_t launch_tree_attn_shared(int head_dim, int nb, int stages, dim3 grid, int threads, size_t lds,
+// bf16 only; a.wr waves of 32 query rows each (nb = 2) in each of kg (1 or 2)
+// key groups, 2-8 waves in all; KV tiles shared through an LDS ring of
+// `stages` (8) K+V tiles
+hipError_t launch_tree_attn_shared(int head_dim, int nb, int stages, int kg, dim3 grid, int threads, size_t lds,
                                    const AttnArgs& a, hipStream_t s, hipEvent_t ev_start = nullptr);
-hipError_t set_tree_attn_shared_lds_limit(int head_dim, int stages, size_t lds);
+hipError_t set_tree_attn_shared_lds_limit(int head_dim, int stages, int kg, size_t lds);
 constexpr int shared_ring_bytes(int head_dim, int stages) { return stages * 2 * kKvTile * head_dim * 2; }
 hipError_t launch_lmhead(int dtype, int mb, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
 constexpr int kLmTileRows = 64;  // vocabulary rows per LM-head workgroup (one statistics tile)
