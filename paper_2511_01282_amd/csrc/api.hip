@@ -24,7 +24,7 @@ struct respec_verify_plan {
   int attn_kg;            // key groups of the shared-tile kernel
   int attn_wg_target;     // workgroups the splits aim for
   size_t attn_lds;
-  // vocabulary statistics: tiles of the LM head and top-K list length
+  // vocabulary statistics: tiles of the LM head and the top-K width (8 or 16)
   int ko, n_vtiles;
   // workspace layout (bytes)
   size_t off_po, off_pm, off_pl, off_x, off_part, off_flag, off_cnt;

@@ -20,7 +20,8 @@
 // token row: 16-byte stores.  When the full step runs, the epilogue also
 // reduces each token row's 64 logits of a statistics tile to its online-softmax
 // statistics {max, sum, entropy sum, argmax} (kTileWords), so that the
-// vocabulary pass reads them instead of the logits.
+// vocabulary pass reads them, and of the logits only the few tiles whose
+// maxima can hold a row's top-K.
 #include <atomic>
 
 #include "common.hpp"
