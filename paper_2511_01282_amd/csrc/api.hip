@@ -277,14 +277,17 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
     lm.vocab = s.vocab;
     lm.hidden_size = s.hidden;
     // token rows per workgroup 16*mb: up to 64 in the plain kernel, 128 or 256 in
-    // the tiled one (bf16), so that W is streamed once for up to 256 rows
+    // the tiled one (bf16), so that W is streamed once for up to 256 rows.  A
+    // vocabulary of more 64-row tiles than two per CU takes 256-row tiles
+    // (bf16): each x row then serves four times as many W rows.
     const int M = a.total_nodes;
     int mb = M <= 16 ? 1 : M <= 32 ? 2 : M <= 48 ? 3 : 4;
     if (M > 64 && s.dtype == RESPEC_BF16) mb = M <= 128 ? 8 : 16;
-    lm.n_mtiles = cdiv(M, 16 * mb);
+    const bool wide = s.dtype == RESPEC_BF16 && M <= 64 && plan->n_vtiles > 2 * kCUs;
+    lm.n_mtiles = wide ? 1 : cdiv(M, 16 * mb);
     lm.partials = full ? reinterpret_cast<float*>(ws + plan->off_part) : nullptr;
     lm.n_vtiles = plan->n_vtiles;
-    if (launch_lmhead(s.dtype, mb, lm, st, ev ? ev[2] : nullptr) != hipSuccess) return RESPEC_ERR_HIP;
+    if (launch_lmhead(s.dtype, mb, wide, lm, st, ev ? ev[2] : nullptr) != hipSuccess) return RESPEC_ERR_HIP;
   } else if (ev && hipEventRecord(ev[2], st) != hipSuccess) {
     return RESPEC_ERR_HIP;
   }

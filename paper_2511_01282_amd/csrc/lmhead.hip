@@ -365,33 +365,36 @@ __global__ __launch_bounds__(256, 2) void lmhead_persistent_kernel(LmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Tiled variant for many token rows (65 to 256 per pass, bf16).  With many
-// token rows the x rows, not W, dominate what a workgroup pulls through its
-// CU, so a workgroup owns 128 vocabulary rows (two statistics tiles), and
-// every byte of W and x it needs crosses the CU once per pass:
-//   - the 128 W rows of a K step go through a double-buffered LDS tile
-//     (requested into registers, 4 pieces of 16 bytes per thread, written to
-//     LDS; one barrier per step), from which every wave reads its A
-//     fragments;
+// Tiled variant (bf16) for many token rows (65 to 256 per pass, 128
+// vocabulary rows per workgroup) and for large vocabularies with up to 64
+// token rows (256 vocabulary rows per workgroup).  There the x rows a
+// workgroup pulls through its CU weigh as much as W or more, so a workgroup
+// owns 16*NVB vocabulary rows (NVB/4 statistics tiles), and every byte of W
+// and x it needs crosses the CU once per pass:
+//   - the W rows of a K step go through a double-buffered LDS tile
+//     (requested into registers, NVB/2 pieces of 16 bytes per thread,
+//     written to LDS; one barrier per step), from which every wave reads its
+//     A fragments;
 //   - wave w owns token rows 16*TB*w .. +16*TB-1 and requests its x fragments
 //     (the B operands) straight into registers; token blocks past the last
 //     row are not multiplied;
 //   - K advances in 128-byte steps through a ring of four register stages:
 //     step c is consumed while steps c+1 .. c+3 are in flight, and step c+4
 //     is requested into the freed registers right after step c's products;
-//   - each wave reduces its token rows over each 64-row half of the tile to
-//     the per-tile statistics.
+//   - each wave reduces its token rows over each 64-row quarter of the tile
+//     to the per-tile statistics.
 constexpr int kTlStep = 128;                 // bytes of a row per K step
 constexpr int kTlPieces = kTlStep / 64;      // mma_k64 calls per K step
 constexpr int kTlWStride = kTlStep + 16;     // LDS row stride of the W tile
-constexpr int kTlRows = 128;                 // vocabulary rows per workgroup
 constexpr int kTlRing = 4;                   // register stages
 
-template <int TB>
+template <int TB, int NVB>
 __device__ __forceinline__ void lmhead_tiled_body(const LmArgs& a) {
-  constexpr int VB = kTlRows / 16;                  // 16-row vocabulary blocks (all waves)
+  constexpr int VB = NVB;                           // 16-row vocabulary blocks (all waves)
+  constexpr int kTlRows = 16 * NVB;                 // vocabulary rows per workgroup
   constexpr int MT = 64 * TB;                       // token rows per workgroup
   constexpr int WP = kTlRows * kTlStep / 16 / 256;  // 16-byte W pieces per thread per step
+  constexpr int NS = kTlRows / kLmTileRows;         // statistics tiles per workgroup
   __shared__ __align__(16) unsigned char sw[2 * kTlRows * kTlWStride];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -399,7 +402,7 @@ __device__ __forceinline__ void lmhead_tiled_body(const LmArgs& a) {
   const int n_mt = a.n_mtiles;
   const int id = blockIdx.x;
   const int grp = id / (8 * n_mt), rem = id % (8 * n_mt);
-  const int vt = grp * 8 + rem % 8, mt = rem / 8;  // vt: 128-row tile
+  const int vt = grp * 8 + rem % 8, mt = rem / 8;  // vt: tile of kTlRows vocabulary rows
   if (vt * kTlRows >= a.vocab) return;
   const int v0 = vt * kTlRows;                     // first vocabulary row of the workgroup
   const int m0 = mt * MT + 16 * TB * wave;         // first token row of this wave
@@ -457,17 +460,20 @@ __device__ __forceinline__ void lmhead_tiled_body(const LmArgs& a) {
     for (int tb = 0; tb < TB; ++tb) acc[vb][tb] = f32x4{0.f, 0.f, 0.f, 0.f};
   auto mma_step = [&](const Stage& st, const unsigned char* buf) {
 #pragma unroll
-    for (int kp = 0; kp < kTlPieces; ++kp) {
-      u32x4 wf[VB];
+    for (int kp = 0; kp < kTlPieces; ++kp)
 #pragma unroll
-      for (int vb = 0; vb < VB; ++vb)
-        wf[vb] = *reinterpret_cast<const u32x4*>(buf + (16 * vb + lr) * kTlWStride + kp * 64 + lg * 16);
+      for (int v0b = 0; v0b < VB; v0b += 8) {  // 8 A fragments at a time
+        u32x4 wf[8];
 #pragma unroll
-      for (int tb = 0; tb < TB; ++tb)
-        if (tb < tbl)
+        for (int vb = 0; vb < 8; ++vb)
+          wf[vb] = *reinterpret_cast<const u32x4*>(buf + (16 * (v0b + vb) + lr) * kTlWStride + kp * 64 + lg * 16);
 #pragma unroll
-          for (int vb = 0; vb < VB; ++vb) acc[vb][tb] = mma_k64(bf16_t{}, wf[vb], st.x[tb][kp], acc[vb][tb]);
-    }
+        for (int tb = 0; tb < TB; ++tb)
+          if (tb < tbl)
+#pragma unroll
+            for (int vb = 0; vb < 8; ++vb)
+              acc[v0b + vb][tb] = mma_k64(bf16_t{}, wf[vb], st.x[tb][kp], acc[v0b + vb][tb]);
+      }
   };
 
   // The steady-state loop only refills real steps (the same count of requests
@@ -519,9 +525,9 @@ __device__ __forceinline__ void lmhead_tiled_body(const LmArgs& a) {
   }
   if (!a.partials) return;
 
-  // per-tile statistics of each token row over each 64-row half of the tile
+  // per-tile statistics of each token row over each 64-row quarter of the tile
 #pragma unroll
-  for (int half = 0; half < 2; ++half) {
+  for (int half = 0; half < NS; ++half) {
     const int vh = v0 + 64 * half;
     if (vh >= a.vocab) break;  // (no statistics tile past V)
 #pragma unroll
@@ -554,15 +560,15 @@ __device__ __forceinline__ void lmhead_tiled_body(const LmArgs& a) {
       st.merge_level<5>();
       const int m = m0 + 16 * tb + lr;
       if (lg == 0 && m < a.m_rows)
-        *reinterpret_cast<u32x4*>(a.partials + ((size_t)m * a.n_vtiles + 2 * vt + half) * kTileWords) =
+        *reinterpret_cast<u32x4*>(a.partials + ((size_t)m * a.n_vtiles + NS * vt + half) * kTileWords) =
             u32x4{__float_as_uint(st.m), __float_as_uint(st.S), __float_as_uint(st.T), (uint32_t)st.am};
     }
   }
 }
 
-template <int TB>
+template <int TB, int NVB>
 __global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
-  lmhead_tiled_body<TB>(a);
+  lmhead_tiled_body<TB, NVB>(a);
 }
 
 // Workgroups of a kernel that fit on the device at once (host occupancy
@@ -606,17 +612,23 @@ static hipError_t launch_mb(int mb, dim3 grid, const LmArgs& a, hipStream_t s, h
   }
 }
 
-hipError_t launch_lmhead(int dtype, int mb, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop) {
+hipError_t launch_lmhead(int dtype, int mb, bool wide, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop) {
   const int n_vt = (a.vocab + kLmRows - 1) / kLmRows;
   const int n_grp = (n_vt + 7) / 8;
   dim3 grid(n_grp * 8 * a.n_mtiles);
   if (mb == 8 || mb == 16) {  // tiled variant: MT = 128 or 256 token rows, 128-row vocabulary tiles (bf16)
     if (dtype != 1) return hipErrorInvalidValue;
-    const int n_vt2 = (a.vocab + kTlRows - 1) / kTlRows;
+    const int n_vt2 = (a.vocab + 127) / 128;
     dim3 tgrid(((n_vt2 + 7) / 8) * 8 * a.n_mtiles);
     const dim3 blk(256);
-    return mb == 8 ? launch_k(lmhead_tiled_kernel<2>, tgrid, blk, 0, s, nullptr, ev_stop, a)
-                   : launch_k(lmhead_tiled_kernel<4>, tgrid, blk, 0, s, nullptr, ev_stop, a);
+    return mb == 8 ? launch_k(lmhead_tiled_kernel<2, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a)
+                   : launch_k(lmhead_tiled_kernel<4, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a);
+  }
+  if (wide) {  // wide tiled variant: up to 64 token rows, 256-row vocabulary tiles (bf16)
+    if (dtype != 1 || mb > 4) return hipErrorInvalidValue;
+    const int n_vt2 = (a.vocab + 255) / 256;
+    dim3 tgrid(((n_vt2 + 7) / 8) * 8 * a.n_mtiles);
+    return launch_k(lmhead_tiled_kernel<1, 16>, tgrid, dim3(256), 0, s, nullptr, ev_stop, a);
   }
   return dtype == 1 ? launch_mb<bf16_t>(mb, grid, a, s, ev_stop) : launch_mb<float>(mb, grid, a, s, ev_stop);
 }
