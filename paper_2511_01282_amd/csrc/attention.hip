@@ -572,11 +572,11 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
     // is clipped to it; so every clamped row below is a valid cache row)
     // (scheduling barriers keep tile 0's loads ahead of tile 1's: the loop's
     // wait counts assume that order)
+    // (tile 1 is requested by the first step, once tile 0's scores are taken:
+    // the wave then starts on tile 0 while tile 1 streams, instead of first
+    // waiting for every request to be accepted)
     load_k_bf16<D>(ka, kbase, tile_row(0), kv_hi, lane);
     load_v_bf16<D>(va, vbase, tile_row(0), kv_hi, lane);
-    __builtin_amdgcn_sched_barrier(0);
-    load_k_bf16<D>(kb, kbase, tile_row(1), kv_hi, lane);
-    load_v_bf16<D>(vb, vbase, tile_row(1), kv_hi, lane);
     __builtin_amdgcn_sched_barrier(0);
     // the tree's own rows (L..) need the ancestor masks: only a split that reaches them
     // waits for the parents (uniform)
@@ -585,9 +585,13 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
     else
       for (int nb = 0; nb < NB; ++nb) anc[nb] = u32x4{0u, 0u, 0u, 0u};
     // one tile: scores from K, V through LDS, then the tile two ahead issued into the freed registers
-    auto tile_step = [&](KTile<D>& kt, VTile<D>& vv, int i, bool refill) {
+    auto tile_step = [&](KTile<D>& kt, VTile<D>& vv, int i, bool refill, bool first) {
       f32x4 s[2][NB];
       scores_bf16<D, NB>(kt, qf, s);
+      if (first) {
+        load_k_bf16<D>(kb, kbase, tile_row(1), kv_hi, lane);
+        load_v_bf16<D>(vb, vbase, tile_row(1), kv_hi, lane);
+      }
       store_v_bf16<D>(vv, vt, lane);
       wave_lds_sync();
       u32x4 vf[DB];
@@ -599,18 +603,20 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
       softmax_pv_bf16<D, NB>(s, vf, t_first + i * t_step, kv_hi, L, qnode, anc, a.scale_log2, m_run, l_run, o, lane);
       wave_lds_sync();  // this tile's V^T reads precede the next tile's writes
     };
-    // Steady state: both halves refill real tiles, so the count of loads behind
-    // every tile is the same on every pass.  The last tiles (straight-line code)
-    // refill only while tiles remain: no load is left in flight for the
-    // workgroup's merge barrier to wait for.
-    int i = 0;
+    // Tile 0, then the steady state from tile 1: both halves refill real
+    // tiles, so the count of loads behind every tile is the same on every
+    // pass.  The last tiles (straight-line code) refill only while tiles
+    // remain: no load is left in flight for the workgroup's merge barrier to
+    // wait for.
+    int i = 1;
+    if (n_tiles > 0) tile_step(ka, va, 0, 2 < n_tiles, true);
     for (; i + 4 <= n_tiles; i += 2) {
-      tile_step(ka, va, i, true);
-      tile_step(kb, vb, i + 1, true);
+      tile_step(kb, vb, i, true, false);
+      tile_step(ka, va, i + 1, true, false);
     }
-    if (i < n_tiles) tile_step(ka, va, i, i + 2 < n_tiles);
-    if (i + 1 < n_tiles) tile_step(kb, vb, i + 1, i + 3 < n_tiles);
-    if (i + 2 < n_tiles) tile_step(ka, va, i + 2, false);
+    if (i < n_tiles) tile_step(kb, vb, i, i + 2 < n_tiles, false);
+    if (i + 1 < n_tiles) tile_step(ka, va, i + 1, i + 3 < n_tiles, false);
+    if (i + 2 < n_tiles) tile_step(kb, vb, i + 2, false, false);
   } else {
     // float32: registers hold one tile; V is transposed through LDS by the VALU
     if (kv_hi > L)
