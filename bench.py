@@ -46,11 +46,14 @@ def stage_bytes(w, M, es):
     kv_rows = sum(int(w.kv_len[b]) + int(w.node_off[b + 1] - w.node_off[b]) for b in range(len(w.kv_len)))
     attn = 2 * s.n_kv_heads * kv_rows * s.head_dim * es + 2 * M * s.hidden * es   # K,V + h in + x out
     lm = s.vocab * s.hidden * es + M * s.hidden * es + M * s.vocab * 4            # W + x + logits out
-    # the LM-head epilogue reduces every 64-logit tile to a partial (m, S, T, argmax and
-    # the top-K keys, K = 8 or 16), so the vocabulary pass reads those, not the logits
+    # the LM-head epilogue reduces every 64-logit tile of a row to 16 bytes of statistics
+    # (m, S, T, argmax); the vocabulary pass reads those, re-reads the K tiles per wave
+    # whose maxima can hold the row's top-K (at least K = 8 or 16 tiles of 256 bytes per
+    # wave, four waves per row past 64 tiles), and reads one logit per child
     n_vtiles = (s.vocab + 63) // 64
     ko = 8 if s.topk_out <= 8 else 16
-    vocab = M * n_vtiles * (4 + 2 * ko) * 4 + M * 4                               # partials + child logits
+    wpr = 4 if n_vtiles > 64 else 1
+    vocab = M * n_vtiles * 16 + M * wpr * ko * 256 + M * 4
     vis = 0
     for b in range(len(w.kv_len)):
         lo, hi = int(w.node_off[b]), int(w.node_off[b + 1])
