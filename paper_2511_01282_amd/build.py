@@ -22,12 +22,22 @@ FLAGS = [
 ]
 
 
+CXX = os.environ.get("CXX", "g++")
+# host-only sources (the drafting side): plain C++, no FP contraction so that the
+# score and entropy arithmetic follows the stated operation order exactly
+CXXFLAGS = ["-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-Wall", "-I", os.path.join(ROOT, "include")]
+
+
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
+def host_sources():
+    return sorted(glob.glob(os.path.join(CSRC, "*.cpp")))
+
+
 def build(verbose: bool = False) -> str:
-    """Compile every HIP source in parallel and link the shared library."""
+    """Compile every HIP and host C++ source in parallel and link the shared library."""
     os.makedirs(OBJ, exist_ok=True)
     procs = []
     objs = []
@@ -35,6 +45,11 @@ def build(verbose: bool = False) -> str:
         obj = os.path.join(OBJ, os.path.basename(src) + ".o")
         objs.append(obj)
         cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+        procs.append((cmd, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
+    for src in host_sources():
+        obj = os.path.join(OBJ, os.path.basename(src) + ".o")
+        objs.append(obj)
+        cmd = [CXX, *CXXFLAGS, "-c", src, "-o", obj]
         procs.append((cmd, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
     failed = []
     for cmd, p in procs:
@@ -46,7 +61,7 @@ def build(verbose: bool = False) -> str:
             print(text)
     if failed:
         msg = "\n\n".join(" ".join(c) + "\n" + t for c, t in failed)
-        raise RuntimeError(f"hipcc failed:\n{msg}")
+        raise RuntimeError(f"compilation failed:\n{msg}")
     tmp = LIB + f".tmp{os.getpid()}"
     subprocess.check_call([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
     os.replace(tmp, LIB)

@@ -106,6 +106,10 @@ EDGE = {
     "d64-bf16-shared-rows": ("bf16", 4, 2, 64, [[-1] + [j // 2 for j in range(0, 47)]], [300]),
     "max-nodes-128": ("bf16", 2, 2, 128, [[-1] + [max(0, j - 4) for j in range(1, 128)]], [31]),
     "max-depth-64": ("bf16", 2, 2, 128, [[-1] + list(range(0, 64))], [5]),
+    # LM-head tiles of 48 and 64 token rows (33-48 and 49-64 nodes) in float32 and bf16
+    "f32-40-nodes": ("f32", 4, 4, 64, [[-1] + [j // 2 for j in range(0, 39)]], [100]),
+    "f32-61-nodes": ("f32", 4, 4, 64, [[-1] + [max(0, j - 3) for j in range(1, 61)]], [77]),
+    "bf16-56-nodes": ("bf16", 4, 2, 128, [[-1] + [j // 3 for j in range(0, 55)]], [64]),
 }
 
 
