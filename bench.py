@@ -87,6 +87,94 @@ def lmhead_traffic(cfg):
     return int(fields["lmhead_traffic_bytes"])
 
 
+def draft_host_timing(seconds=1.0):
+    """Host cost of the drafting side of a step (trigger, suffix-automaton retrieval, EMA
+    selection, BuildDraftTree, then feedback and context append), library against oracle.
+
+    Scenario (copy-heavy, like summarisation or retrieval-augmented generation): a context
+    of 8192 synthetic tokens (Zipf(1.1) over a 32000 vocabulary) and an output that copies
+    the span starting at token 1000 with one token in ten replaced.  Every token's entropy
+    is 0.5 nats, so the trigger fires.  Each round proposes a tree; the stand-in verifier
+    accepts the tree's longest greedy match of the output, the bonus is the output's next
+    token, and the round commits.  Only the library calls (propose, commit through the
+    C ABI, buffers allocated once) and the oracle's propose and commit are timed; both run
+    the same rounds, so their accepted lengths must agree.
+    """
+    import ctypes
+    import numpy as np
+    import respec_synth as synth
+    from paper_2511_01282_amd import draft
+    import oracle.draft as od
+
+    n, V = 8192, 32000
+    cdf = np.cumsum(np.arange(1, V + 1, dtype=np.float64) ** -1.1)
+    cdf /= cdf[-1]
+    ctx = np.searchsorted(cdf, synth.uniform_stream(9, 40, 0, n)).astype(np.int32)
+    out = ctx[1000:1000 + 4000].copy()
+    sub = synth.uniform_stream(9, 41, 0, len(out)) < 0.1
+    out[sub] = np.searchsorted(cdf, synth.uniform_stream(9, 42, 0, len(out)))[sub]
+    ent = np.full(n, 0.5, np.float32)
+
+    def outcome(parent, token, pos):
+        """Greedy match of the output along the tree: the accepted path and the bonus token."""
+        kids = {}
+        for j in range(1, len(parent)):
+            kids.setdefault(int(parent[j]), []).append(j)
+        path, v = [0], 0
+        while pos + len(path) - 1 < len(out):
+            nxt = [c for c in kids.get(v, []) if token[c] == out[pos + len(path) - 1]]
+            if not nxt:
+                break
+            v = nxt[0]
+            path.append(v)
+        acc = len(path) - 1
+        return path, acc, int(out[min(pos + acc, len(out) - 1)])
+
+    L = draft.lib()
+    sess = draft.DraftSession()
+    sess.append(ctx, ent)
+    cap = sess.params.tree.max_nodes
+    parent, token = np.empty(cap, np.int32), np.empty(cap, np.int32)
+    src, res = np.empty(cap, np.uint8), draft.DraftResult()
+    path_buf = np.empty(cap, np.int32)
+    node_ent = np.full(cap, 0.5, np.float32)
+    h, pp, tp, sp = sess._h, parent.ctypes.data, token.ctypes.data, src.ctypes.data
+    lib_acc, t_lib, pos = [], 0.0, 0
+    while (t_lib < seconds / 2 or len(lib_acc) < 20) and pos < len(out) - 64:
+        t0 = time.perf_counter()
+        st = L.respec_draft_session_propose(h, pp, tp, sp, cap, ctypes.byref(res))
+        t_lib += time.perf_counter() - t0
+        m = res.n_nodes
+        path, acc, bonus = outcome(parent[:m], token[:m], pos)
+        path_buf[:acc + 1] = path
+        t0 = time.perf_counter()
+        st |= L.respec_draft_session_commit(h, tp, path_buf.ctypes.data, acc, bonus, node_ent.ctypes.data)
+        t_lib += time.perf_counter() - t0
+        if st:
+            raise RuntimeError("drafting session call failed")
+        lib_acc.append(acc)
+        pos += acc + 1
+    o = od.Session()
+    o.append([int(v) for v in ctx], [float(v) for v in ent])
+    or_acc, t_or, pos = [], 0.0, 0
+    e_list = [0.5] * cap
+    while len(or_acc) < len(lib_acc) and (t_or < seconds / 2 or len(or_acc) < 5):
+        t0 = time.perf_counter()
+        r = o.propose()
+        t_or += time.perf_counter() - t0
+        path, acc, bonus = outcome(r["parent"], r["token"], pos)
+        t0 = time.perf_counter()
+        o.commit(r["token"], path, acc, bonus, e_list)
+        t_or += time.perf_counter() - t0
+        or_acc.append(acc)
+        pos += acc + 1
+    return {"us_per_step": round(t_lib / len(lib_acc) * 1e6, 2), "rounds": len(lib_acc),
+            "mean_accepted": round(float(np.mean(lib_acc)), 3), "context_tokens": n,
+            "oracle_us_per_step": round(t_or / len(or_acc) * 1e6, 1), "oracle_rounds": len(or_acc),
+            "oracle_agrees": or_acc == lib_acc[:len(or_acc)],
+            "what": "propose (trigger, retrieval, selection, tree) + commit (EMA, append), host, 1 thread"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -224,6 +312,8 @@ def main():
                "sample": f"{n_done} full steps of the same workload (attention, LM head, vocab statistics, "
                          f"acceptance, path), float64, {t_cpu:.1f} s"}
 
+    draft_host = None if args.no_cpu_baseline else draft_host_timing()
+
     wl = {"workload": f"{shp.name}: {shp.dtype}, hidden {shp.hidden}, heads {shp.n_q_heads}/{shp.n_kv_heads}, "
                       f"head_dim {shp.head_dim}, vocab {shp.vocab}, batch {B}, nodes {M}, "
                       f"KV len {int(w.kv_len.max())}", "config_index": cfg, "rotated_input_sets": R}
@@ -232,7 +322,7 @@ def main():
         "value": round(K / wall, 2), "unit": "steps/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if shp.dtype == "bf16" else "f32", "data": "synthetic", "config": wl,
-        "roofline": roofline, "cpu_baseline": cpu,
+        "roofline": roofline, "cpu_baseline": cpu, "draft_host": draft_host,
         "stages": {k: ({kk: round(vv, 3) for kk, vv in v.items()} if isinstance(v, dict) else round(v, 3))
                    for k, v in stages.items()},
         "device": torch.cuda.get_device_name(dev),

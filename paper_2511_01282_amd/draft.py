@@ -141,9 +141,12 @@ class Sam:
             self.extend(tokens)
 
     def __del__(self):
-        if getattr(self, "_own", False) and getattr(self, "_h", None):
-            lib().respec_sam_destroy(self._h)
-            self._h = None
+        try:
+            if getattr(self, "_own", False) and getattr(self, "_h", None):
+                lib().respec_sam_destroy(self._h)
+                self._h = None
+        except Exception:   # interpreter shutdown
+            pass
 
     def extend(self, tokens) -> None:
         t = _i32(tokens)
@@ -184,9 +187,12 @@ class Scores:
             self._h = _P(_view)
 
     def __del__(self):
-        if getattr(self, "_own", False) and getattr(self, "_h", None):
-            lib().respec_scores_destroy(self._h)
-            self._h = None
+        try:
+            if getattr(self, "_own", False) and getattr(self, "_h", None):
+                lib().respec_scores_destroy(self._h)
+                self._h = None
+        except Exception:   # interpreter shutdown
+            pass
 
     def get(self, pos: int, s0: float = 0.5) -> float:
         return float(lib().respec_scores_get(self._h, int(pos), float(s0)))
@@ -261,9 +267,12 @@ class DraftSession:
         self.scores = Scores(_view=lib().respec_draft_session_scores(h))
 
     def __del__(self):
-        if getattr(self, "_h", None):
-            lib().respec_draft_session_destroy(self._h)
-            self._h = None
+        try:
+            if getattr(self, "_h", None):
+                lib().respec_draft_session_destroy(self._h)
+                self._h = None
+        except Exception:   # interpreter shutdown
+            pass
 
     def append(self, tokens, entropy=None) -> None:
         t = _i32(tokens)
