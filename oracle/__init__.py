@@ -65,6 +65,10 @@ def _lib():
             "respec_oracle_threads": (_I32, []),
             "respec_oracle_path": (None, [_I32, _P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P,
                                           _P, _P, _P]),
+            "respec_oracle_stoch_node": (_I32, [_I32, _P, ctypes.c_float, _P, _I32, _P, _P, _P,
+                                                ctypes.c_float, _P]),
+            "respec_oracle_stochastic": (_I32, [_I32, _P, _P, _P, _P, _I32, _P, _P, ctypes.c_float, _I32,
+                                                _P, _P, _P, _P, _P, _P, _P, _P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(lib, name)
@@ -201,6 +205,41 @@ def path(parent, is_leaf, depth, flags, argmax, max_depth: int, m: int, phi: int
                               max_depth, m, phi, _p(leaf_acc), _p(pth), _p(acc), _p(bonus), _p(wl))
     return dict(leaf_acc_len=leaf_acc, path=pth, acc_len=int(acc[0]), bonus=int(bonus[0]),
                 winner_leaf=int(wl[0]))
+
+
+def stoch_node(z_row, temperature: float, q_row, child_tok, child_model, u_acc, u_res: float):
+    """One node of stochastic verification: (first accepted child index or -1, residual draw or -1)."""
+    z = _c(z_row, np.float32)
+    q = None if q_row is None else _c(q_row, np.float32)
+    ct = _c(child_tok, np.int32) if len(child_tok) else np.zeros(1, np.int32)
+    cm = _c(child_model, np.uint8) if len(child_model) else np.zeros(1, np.uint8)
+    ua = _c(u_acc, np.float32) if len(u_acc) else np.zeros(1, np.float32)
+    smp = np.zeros(1, np.int32)
+    k = _lib().respec_oracle_stoch_node(z.shape[0], _p(z), float(temperature), None if q is None else _p(q),
+                                        len(child_tok), _p(ct), _p(cm), _p(ua), float(u_res), _p(smp))
+    return int(k), int(smp[0])
+
+
+def stochastic(parent, token, src, z32, q, u, temperature: float, max_depth: int):
+    """Stochastic verification of one sequence's tree (None for a malformed tree)."""
+    parent = _c(parent, np.int32)
+    token = _c(token, np.int32)
+    src = _c(src, np.uint8)
+    z32 = _c(z32, np.float32)
+    q = None if q is None else _c(q, np.float32)
+    u = _c(u, np.float32)
+    n, V = z32.shape
+    out = dict(first_acc=np.zeros(n, np.int32), sample=np.zeros(n, np.int32), acc_bit=np.zeros(n, np.uint8),
+               path=np.zeros(max_depth + 1, np.int32), leaf_acc_len=np.zeros(n, np.int32))
+    acc, bonus, wl = np.zeros(1, np.int32), np.zeros(1, np.int32), np.zeros(1, np.int32)
+    st = _lib().respec_oracle_stochastic(n, _p(parent), _p(token), _p(src), _p(z32), V,
+                                         None if q is None else _p(q), _p(u), float(temperature), max_depth,
+                                         _p(out["first_acc"]), _p(out["sample"]), _p(out["acc_bit"]),
+                                         _p(out["path"]), _p(acc), _p(bonus), _p(wl), _p(out["leaf_acc_len"]))
+    if st != 0:
+        return None
+    out.update(acc_len=int(acc[0]), bonus=int(bonus[0]), winner_leaf=int(wl[0]))
+    return out
 
 
 # ---------------------------------------------------------------------------

@@ -26,12 +26,21 @@
  *    are taken on logits rounded to float32, the precision the GPU kernel
  *    stores them in.
  *
+ *  - stochastic verification (drafter outputs verified by lossless
+ *    speculative sampling, Section 3.4) tries a node's children in index
+ *    order, each against the residual left by the rejected ones; a retrieved
+ *    child is a deterministic draft (one-hot draft distribution).
+ *
  * Parity pins (tests): chain trees against textbook causal attention, star
  * trees against decode attention, logits against a library GEMM, entropy and
  * log-sum-exp against library routines and closed forms, top-k against a full
  * stable sort, hand-worked look-ahead cases, brute-force path enumeration.
  * The look-ahead reading itself has no worked example in the paper: parity of
  * that step is unpinned beyond the hand-worked cases derived from the prose.
+ * Stochastic verification: hand-worked acceptance probabilities and residual
+ * draws, Monte Carlo losslessness (the emitted token follows the target
+ * distribution), a drafter equal to the target, and the vanishing-temperature
+ * limit against greedy verification.
  */
 #include <math.h>
 #include <omp.h>
@@ -370,4 +379,166 @@ void respec_oracle_path(int32_t n, const int32_t* parent, const uint8_t* is_leaf
     free(chain);
     free(g);
     free(ok);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Stochastic (lossless) verification.  Section 3.4 verifies drafter outputs
+ * with standard lossless speculative sampling: a draft token t drawn from the
+ * drafter's distribution q is accepted with probability min(1, p(t) / q(t))
+ * under the target's distribution p; on rejection the next token is drawn
+ * from the residual norm(max(p - q, 0)).  A tree node with several children
+ * tries them in order (recursive rejection over siblings, the multi-draft
+ * form of the same rule): child k is tested against the residual r left by
+ * the rejection of children 1..k-1, and each rejection replaces r by
+ * norm(max(r - q_k, 0)).  A model-drafted child uses the drafter's
+ * distribution at its parent; a retrieved child is a deterministic draft,
+ * q_k = one-hot at its token.  Random numbers are inputs: u_acc[k] decides
+ * child k (accept iff u < a), u_res the residual draw (inverse CDF: the
+ * smallest v whose cumulative residual mass exceeds u_res times the total).
+ * Everything in double; p = softmax(z / T) from the float32 logits.
+ *
+ * One node: returns the index of the first accepted child, or -1 when every
+ * child is rejected, in which case *sample receives the residual draw (else
+ * -1).  q_row may be NULL: every child is then a deterministic draft.
+ * If a rejection leaves no residual mass (r = q_k), r is kept as it was.   */
+int32_t respec_oracle_stoch_node(int32_t vocab, const float* z_row, float temperature, const float* q_row,
+                                 int32_t n_child, const int32_t* child_tok, const uint8_t* child_model,
+                                 const float* u_acc, float u_res, int32_t* sample) {
+    double* r = (double*)malloc(sizeof(double) * (size_t)vocab);
+    const double T = (double)temperature;
+    double m = -INFINITY, s = 0.0;
+    for (int32_t v = 0; v < vocab; ++v)
+        if ((double)z_row[v] > m) m = (double)z_row[v];
+    for (int32_t v = 0; v < vocab; ++v) {
+        r[v] = exp(((double)z_row[v] - m) / T);
+        s += r[v];
+    }
+    for (int32_t v = 0; v < vocab; ++v) r[v] /= s;          /* p = softmax(z / T) */
+    int32_t accepted = -1;
+    for (int32_t k = 0; k < n_child && accepted < 0; ++k) {
+        const int32_t t = child_tok[k];
+        const int model = child_model[k] && q_row != NULL;
+        const double qt = model ? (double)q_row[t] : 1.0;
+        const double rt = r[t];
+        const double a = qt > 0.0 ? (rt / qt < 1.0 ? rt / qt : 1.0) : (rt > 0.0 ? 1.0 : 0.0);
+        if ((double)u_acc[k] < a) {
+            accepted = k;
+            break;
+        }
+        double z = 0.0;
+        for (int32_t v = 0; v < vocab; ++v) {
+            const double qv = model ? (double)q_row[v] : (v == t ? 1.0 : 0.0);
+            const double d = r[v] - qv;
+            z += d > 0.0 ? d : 0.0;
+        }
+        if (z > 0.0)
+            for (int32_t v = 0; v < vocab; ++v) {
+                const double qv = model ? (double)q_row[v] : (v == t ? 1.0 : 0.0);
+                const double d = r[v] - qv;
+                r[v] = d > 0.0 ? d / z : 0.0;
+            }
+    }
+    *sample = -1;
+    if (accepted < 0) {
+        double total = 0.0;
+        for (int32_t v = 0; v < vocab; ++v) total += r[v];
+        const double thr = (double)u_res * total;
+        double c = 0.0;
+        int32_t last_pos = 0;
+        for (int32_t v = 0; v < vocab; ++v) {
+            if (r[v] > 0.0) last_pos = v;
+            c += r[v];
+            if (c > thr) {
+                *sample = v;
+                break;
+            }
+        }
+        if (*sample < 0) *sample = last_pos;
+    }
+    free(r);
+    return accepted;
+}
+
+/* Stochastic verification of one sequence's tree.  Children of a node are
+ * tried in node-index order.  Per node i: first_acc[i] = the first accepted
+ * child (global to the sequence, -1 if none), sample[i] = the residual draw
+ * when no child is accepted (else -1), acc_bit[j] = 1 iff j is the first
+ * accepted child of its parent.  The walk starts at the root and moves to the
+ * first accepted child until none is: path = the walked nodes (root first,
+ * -1 padded to max_depth+1), acc_len = their count - 1, bonus = the residual
+ * draw at the last one, winner_leaf = the smallest leaf whose chain holds the
+ * last one, leaf_acc[l] = the number of walked non-root nodes on leaf l's
+ * chain (-1 for inner nodes).  u holds two uniforms per node: [j][0] tests
+ * node j as a child, [j][1] draws at node j.  q is [n][V] (row i: the
+ * drafter's distribution at node i) or NULL.  Returns 0, or 1 for a tree
+ * that respec_oracle_tree rejects (outputs untouched).                       */
+int respec_oracle_stochastic(int32_t n, const int32_t* parent, const int32_t* token, const uint8_t* src,
+                             const float* z32, int32_t vocab, const float* q, const float* u, float temperature,
+                             int32_t max_depth, int32_t* first_acc, int32_t* sample, uint8_t* acc_bit,
+                             int32_t* path, int32_t* acc_len, int32_t* bonus, int32_t* winner_leaf,
+                             int32_t* leaf_acc) {
+    int32_t* depth = (int32_t*)malloc(sizeof(int32_t) * (size_t)n);
+    uint8_t* anc = (uint8_t*)malloc((size_t)n * (size_t)n);
+    uint8_t* is_leaf = (uint8_t*)malloc((size_t)n);
+    if (respec_oracle_tree(parent, n, max_depth, depth, anc, is_leaf) != 0) {
+        free(depth);
+        free(anc);
+        free(is_leaf);
+        return 1;
+    }
+    int32_t* kids = (int32_t*)malloc(sizeof(int32_t) * (size_t)n);
+    int32_t* ktok = (int32_t*)malloc(sizeof(int32_t) * (size_t)n);
+    uint8_t* kmodel = (uint8_t*)malloc((size_t)n);
+    float* kuacc = (float*)malloc(sizeof(float) * (size_t)n);
+    for (int32_t j = 0; j < n; ++j) acc_bit[j] = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        int32_t nk = 0;
+        for (int32_t j = i + 1; j < n; ++j)
+            if (parent[j] == i) {
+                kids[nk] = j;
+                ktok[nk] = token[j];
+                kmodel[nk] = src[j] != SRC_RETRIEVED;
+                kuacc[nk] = u[2 * (size_t)j];
+                ++nk;
+            }
+        const int32_t k = respec_oracle_stoch_node(vocab, z32 + (size_t)i * vocab, temperature,
+                                                   q ? q + (size_t)i * vocab : NULL, nk, ktok, kmodel, kuacc,
+                                                   u[2 * (size_t)i + 1], &sample[i]);
+        first_acc[i] = k >= 0 ? kids[k] : -1;
+        if (k >= 0) acc_bit[kids[k]] = 1;
+    }
+    /* the walk */
+    uint8_t* walked = (uint8_t*)calloc((size_t)n, 1);
+    for (int32_t d = 0; d <= max_depth; ++d) path[d] = -1;
+    int32_t cur = 0, len = 0;
+    walked[0] = 1;
+    path[0] = 0;
+    while (first_acc[cur] >= 0) {
+        cur = first_acc[cur];
+        walked[cur] = 1;
+        path[++len] = cur;
+    }
+    *acc_len = len;
+    *bonus = sample[cur];
+    *winner_leaf = -1;
+    for (int32_t l = 0; l < n; ++l) {
+        if (!is_leaf[l]) {
+            leaf_acc[l] = -1;
+            continue;
+        }
+        int32_t c = 0;
+        for (int32_t a = 1; a < n; ++a)
+            if (anc[(size_t)l * n + a] && walked[a]) ++c;
+        leaf_acc[l] = c;
+        if (*winner_leaf < 0 && anc[(size_t)l * n + cur]) *winner_leaf = l;
+    }
+    free(walked);
+    free(kids);
+    free(ktok);
+    free(kmodel);
+    free(kuacc);
+    free(depth);
+    free(anc);
+    free(is_leaf);
+    return 0;
 }
