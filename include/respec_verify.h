@@ -69,7 +69,9 @@ enum {
   RESPEC_FLAG_TOPK = 2,     /* t_j in TopK_k(p_i), ties by smaller token id (Eq. 6)         */
   RESPEC_FLAG_TAU = 4,      /* log p_i(argmax) - log p_i(t_j) <= tau (Eq. 7)                */
   RESPEC_FLAG_RELAXED = 8,  /* src_j == RETRIEVED and TOPK and TAU                          */
-  RESPEC_FLAG_ON_PATH = 16  /* node is on the accepted path (the root always is)            */
+  RESPEC_FLAG_ON_PATH = 16, /* node is on the accepted path (the root always is)            */
+  RESPEC_FLAG_STOCH_ACCEPT = 32 /* stochastic mode: the first child of its parent that passes
+                                   the speculative-sampling test (see respec_accept_params)   */
 };
 
 /* stop_after (debugging and per-stage timing) */
@@ -93,12 +95,33 @@ typedef struct {
   int32_t topk_out;    /* width of the top-k output, 1..RESPEC_MAX_TOPK_OUT                */
 } respec_verify_shape;
 
-/* Acceptance parameters (Section 3.4), per call. */
+/* Acceptance parameters (Section 3.4), per call.
+ *
+ * stochastic = 0 (the paper's experiments): model-drafted nodes are verified
+ * strictly and greedily (token == argmax), retrieved nodes with the relaxed
+ * check and the look-ahead tolerance procedure; the longest accepted chain wins.
+ *
+ * stochastic = 1: lossless speculative sampling (Section 3.4, drafter outputs)
+ * at temperature T, p = softmax(z / T).  A node tries its children in node
+ * order; child j passes with probability min(1, r(t_j) / q_j(t_j)), decided by
+ * uniform[j][0] < that probability, where r is the node's p with the residual
+ * of every earlier rejected sibling k applied, r <- norm(max(r - q_k, 0)) (kept
+ * as it is when that has no mass).  q_j is row i of draft_prob for a MODEL
+ * child of node i and one-hot at t_j for a RETRIEVED child (a deterministic
+ * draft; also for every child when draft_prob is NULL).  The walk starts at the
+ * root and moves to the first passing child until none passes; path, acc_len
+ * and ON_PATH describe it, bonus is the residual draw at its last node (the
+ * smallest token whose cumulative residual mass exceeds uniform[i][1] times
+ * the total), winner_leaf the smallest leaf below that node, leaf_acc_len the
+ * walked nodes on each leaf's chain.  GREEDY/TOPK/TAU/RELAXED are still
+ * reported (at T = 1), and so are the statistics. */
 typedef struct {
   int32_t topk;          /* k of TopK_k, 1 <= k <= topk_out                               */
   float tau;             /* tolerance margin, >= 0 (in nats = logit units)                 */
   int32_t min_lookahead; /* m: greedy matches required after a relaxed token, >= 0         */
   int32_t max_relaxed;   /* Phi: relaxed attempts per candidate chain, >= 0                */
+  int32_t stochastic;    /* 0: greedy strict / relaxed verification; 1: speculative sampling */
+  float temperature;     /* T of stochastic verification, finite and > 0                   */
 } respec_accept_params;
 
 typedef struct {
@@ -126,6 +149,11 @@ typedef struct {
   const int32_t* token;     /* [M] int32 draft token of each node in [0, V); the root's
                                entry is not checked                                        */
   const uint8_t* src;       /* [M] uint8 respec_src of each node                            */
+  const float* draft_prob;  /* stochastic only: [M][V] float32, row i = the drafter's
+                               distribution at node i (that its MODEL children were drawn
+                               from), 16-byte aligned; NULL = every draft deterministic     */
+  const float* uniform;     /* stochastic only (required): [M][2] float32 uniforms in [0,1):
+                               [j][0] tests node j as a child, [j][1] draws at node j       */
 
   /* outputs (device) */
   float* attn_out;          /* [M][Hd] float32 attention output O, or NULL                 */
@@ -145,6 +173,8 @@ typedef struct {
   int32_t* bonus;           /* [B] argmax at the last accepted node (the free token)       */
   int32_t* winner_leaf;     /* [B] sequence-local leaf whose chain won, -1 on error         */
   int32_t* seq_status;      /* [B] RESPEC_OK, RESPEC_ERR_TREE or RESPEC_ERR_TOKEN           */
+  int32_t* sample;          /* stochastic, optional: [M] the residual draw at node i when no
+                               child of i passes, else -1 (NULL = not written)             */
 
   void* stage_events;       /* optional host array of 4 hipEvent_t (profiling), NULL = none:
                                [0] start of the attention kernel, [1] end of the split

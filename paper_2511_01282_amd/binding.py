@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "librespec_verify.so")
 OK, ERR_NULL, ERR_SHAPE, ERR_DTYPE, ERR_PARAM, ERR_TREE, ERR_CAPACITY, ERR_HIP, ERR_WORKSPACE, ERR_TOKEN = range(10)
 F32, BF16 = 0, 1
 SRC_MODEL, SRC_RETRIEVED = 0, 1
-FLAG_GREEDY, FLAG_TOPK, FLAG_TAU, FLAG_RELAXED, FLAG_ON_PATH = 1, 2, 4, 8, 16
+FLAG_GREEDY, FLAG_TOPK, FLAG_TAU, FLAG_RELAXED, FLAG_ON_PATH, FLAG_STOCH_ACCEPT = 1, 2, 4, 8, 16, 32
 STOP_ALL, STOP_ATTN, STOP_LOGITS = 0, 1, 2
 MAX_NODES, MAX_DEPTH, MAX_TOPK_OUT = 128, 64, 16
 
@@ -37,7 +37,8 @@ class Shape(ctypes.Structure):
 
 class AcceptParams(ctypes.Structure):
     _fields_ = [("topk", ctypes.c_int32), ("tau", ctypes.c_float),
-                ("min_lookahead", ctypes.c_int32), ("max_relaxed", ctypes.c_int32)]
+                ("min_lookahead", ctypes.c_int32), ("max_relaxed", ctypes.c_int32),
+                ("stochastic", ctypes.c_int32), ("temperature", ctypes.c_float)]
 
 
 _P = ctypes.c_void_p
@@ -50,18 +51,19 @@ class Args(ctypes.Structure):
         ("kv_capacity", ctypes.c_int32), ("stop_after", ctypes.c_int32),
         ("accept", AcceptParams),
         ("node_off", _P), ("kv_len", _P), ("hidden", _P), ("k_cache", _P), ("v_cache", _P),
-        ("lm_head", _P), ("parent", _P), ("token", _P), ("src", _P),
+        ("lm_head", _P), ("parent", _P), ("token", _P), ("src", _P), ("draft_prob", _P), ("uniform", _P),
         ("attn_out", _P), ("logits", _P), ("max_logit", _P), ("lse", _P), ("entropy", _P),
         ("argmax", _P), ("topk_id", _P), ("topk_logprob", _P), ("tok_logprob", _P), ("flags", _P),
         ("leaf_acc_len", _P), ("path", _P), ("acc_len", _P), ("bonus", _P), ("winner_leaf", _P),
-        ("seq_status", _P), ("stage_events", _P),
+        ("seq_status", _P), ("sample", _P), ("stage_events", _P),
     ]
 
 
-INPUT_FIELDS = ("node_off", "kv_len", "hidden", "k_cache", "v_cache", "lm_head", "parent", "token", "src")
+INPUT_FIELDS = ("node_off", "kv_len", "hidden", "k_cache", "v_cache", "lm_head", "parent", "token", "src",
+                "draft_prob", "uniform")
 OUTPUT_FIELDS = ("attn_out", "logits", "max_logit", "lse", "entropy", "argmax", "topk_id", "topk_logprob",
                  "tok_logprob", "flags", "leaf_acc_len", "path", "acc_len", "bonus", "winner_leaf",
-                 "seq_status")
+                 "seq_status", "sample")
 
 _LIB = None
 
@@ -169,13 +171,13 @@ class Plan:
 
     def step(self, inputs: dict, outputs: dict, *, batch, total_nodes, max_nodes_in_batch,
              max_kv_len_in_batch, kv_capacity, topk=8, tau=3.0, min_lookahead=2, max_relaxed=2,
-             stop_after=STOP_ALL, stream=None, stage_events=None) -> None:
+             stochastic=0, temperature=1.0, stop_after=STOP_ALL, stream=None, stage_events=None) -> None:
         """Enqueue one verification step (asynchronous, on ``stream``)."""
         a = Args()
         a.batch, a.total_nodes = batch, total_nodes
         a.max_nodes_in_batch, a.max_kv_len_in_batch = max_nodes_in_batch, max_kv_len_in_batch
         a.kv_capacity, a.stop_after = kv_capacity, stop_after
-        a.accept = AcceptParams(topk, tau, min_lookahead, max_relaxed)
+        a.accept = AcceptParams(topk, tau, min_lookahead, max_relaxed, int(stochastic), temperature)
         for f in INPUT_FIELDS:
             setattr(a, f, _ptr(inputs.get(f)))
         for f in OUTPUT_FIELDS:
@@ -203,4 +205,5 @@ def alloc_outputs(*, total_nodes, batch, hidden, vocab, topk_out, max_depth, dev
         "leaf_acc_len": torch.empty(M, **i32), "path": torch.empty(B, max_depth + 1, **i32),
         "acc_len": torch.empty(B, **i32), "bonus": torch.empty(B, **i32),
         "winner_leaf": torch.empty(B, **i32), "seq_status": torch.empty(B, **i32),
+        "sample": torch.empty(M, **i32),
     }

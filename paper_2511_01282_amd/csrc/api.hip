@@ -27,7 +27,7 @@ struct respec_verify_plan {
   // vocabulary statistics: tiles of the LM head and the top-K width (8 or 16)
   int ko, n_vtiles;
   // workspace layout (bytes)
-  size_t off_po, off_pm, off_pl, off_x, off_part, off_flag, off_cnt;
+  size_t off_po, off_pm, off_pl, off_x, off_part, off_flag, off_cnt, off_stoch;
   size_t n_cnt_seq, total;
   // the attention kernel's LDS limit is raised on the first step (plan creation stays GPU-free)
   mutable std::atomic<bool> lds_ready{false};
@@ -157,6 +157,7 @@ respec_status respec_verify_create(const respec_verify_shape* shape, respec_veri
   p->off_flag = off; off = align256(off + mcap * 4);
   p->n_cnt_seq = s.max_batch;
   p->off_cnt = off; off = align256(off + p->n_cnt_seq * 4);
+  p->off_stoch = off; off = align256(off + 2 * mcap * 4);  // stochastic walk: next child, draw
   p->total = off;
 
   *out = p;
@@ -189,9 +190,11 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   if (full) {
     const respec_accept_params& q = a.accept;
     if (q.topk < 1 || q.topk > s.topk_out || !(q.tau >= 0.f) || isinf(q.tau) || q.min_lookahead < 0 ||
-        q.max_relaxed < 0)
+        q.max_relaxed < 0 || (q.stochastic != 0 && q.stochastic != 1))
       return RESPEC_ERR_PARAM;
+    if (q.stochastic && (!(q.temperature > 0.f) || isinf(q.temperature))) return RESPEC_ERR_PARAM;
   }
+  const bool stochastic = full && a.accept.stochastic;
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipEvent_t* ev = static_cast<hipEvent_t*>(a.stage_events);
   if (a.batch == 0) {
@@ -211,6 +214,8 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
                !a.topk_logprob || !a.tok_logprob || !a.flags || !a.leaf_acc_len || !a.path || !a.acc_len ||
                !a.bonus || !a.winner_leaf || !a.seq_status))
     return RESPEC_ERR_NULL;
+  if (stochastic && !a.uniform) return RESPEC_ERR_NULL;
+  if (stochastic && a.draft_prob && !aligned(a.draft_prob, 16)) return RESPEC_ERR_SHAPE;
   if (!aligned(a.hidden, 16) || !aligned(a.k_cache, 16) || !aligned(a.v_cache, 16) ||
       (need_logits && (!aligned(a.lm_head, 16) || !aligned(a.logits, 16))) || (a.attn_out && !aligned(a.attn_out, 16)))
     return RESPEC_ERR_SHAPE;
@@ -331,8 +336,41 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
     v.min_lookahead = a.accept.min_lookahead;
     v.max_relaxed = a.accept.max_relaxed;
     v.tau = a.accept.tau;
-    if (launch_finalize(plan->ko, a.total_nodes + a.batch, v, st, ev ? ev[3] : nullptr) != hipSuccess)
+    if (launch_finalize(plan->ko, a.total_nodes + a.batch, v, st, (ev && !stochastic) ? ev[3] : nullptr) !=
+        hipSuccess)
       return RESPEC_ERR_HIP;
+    if (stochastic) {
+      // speculative-sampling walk, after the row statistics and the tree checks
+      StochArgs sa;
+      sa.logits = a.logits;
+      sa.max_logit = a.max_logit;
+      sa.lse = a.lse;
+      sa.draft_prob = a.draft_prob;
+      sa.uniform = a.uniform;
+      sa.node_off = a.node_off;
+      sa.parent = a.parent;
+      sa.token = a.token;
+      sa.src = a.src;
+      sa.seq_status = a.seq_status;
+      sa.seq_counter = cnt;
+      sa.ws_next = reinterpret_cast<int32_t*>(ws + plan->off_stoch);
+      sa.ws_sample = sa.ws_next + (size_t)s.max_batch * s.max_nodes;
+      sa.flags = a.flags;
+      sa.sample = a.sample;
+      sa.leaf_acc_len = a.leaf_acc_len;
+      sa.path = a.path;
+      sa.acc_len = a.acc_len;
+      sa.bonus = a.bonus;
+      sa.winner_leaf = a.winner_leaf;
+      sa.total_nodes = a.total_nodes;
+      sa.batch = a.batch;
+      sa.vocab = s.vocab;
+      sa.max_nodes = a.max_nodes_in_batch;
+      sa.max_depth = s.max_depth;
+      sa.inv_temp = 1.f / a.accept.temperature;
+      sa.unit_temp = a.accept.temperature == 1.f;
+      if (launch_stochastic(sa, st, ev ? ev[3] : nullptr) != hipSuccess) return RESPEC_ERR_HIP;
+    }
   } else if (ev && hipEventRecord(ev[3], st) != hipSuccess) {
     return RESPEC_ERR_HIP;
   }

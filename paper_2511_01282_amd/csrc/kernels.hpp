@@ -60,6 +60,28 @@ struct VocabArgs {
   float tau;
 };
 
+struct StochArgs {
+  const float* logits;     // [M][V]
+  const float* max_logit;  // [M] (vocabulary pass)
+  const float* lse;        // [M] (vocabulary pass)
+  const float* draft_prob; // [M][V] drafter distribution at each node, or null (every draft deterministic)
+  const float* uniform;    // [M][2]
+  const int32_t* node_off; // [B+1]
+  const int32_t* parent;
+  const int32_t* token;
+  const uint8_t* src;
+  const int32_t* seq_status;  // [B] (vocabulary pass)
+  int32_t* seq_counter;    // [B], zero between steps
+  int32_t* ws_next;        // [M] first accepted child of each node (sequence-local) or -1
+  int32_t* ws_sample;      // [M] residual draw of each node or -1
+  // outputs
+  uint8_t* flags; int32_t* sample; int32_t* leaf_acc_len; int32_t* path; int32_t* acc_len; int32_t* bonus;
+  int32_t* winner_leaf;
+  int32_t total_nodes, batch, vocab, max_nodes, max_depth;
+  float inv_temp;          // 1 / T
+  int32_t unit_temp;       // T == 1: the normaliser comes from the log-sum-exp
+};
+
 // Launch a kernel whose single argument is an argument struct.  Optional
 // start / stop events take the dispatch's own timestamps (hipExtLaunchKernel),
 // so a stage timed with them matches the kernel's duration.
@@ -97,6 +119,7 @@ constexpr int kLmTileRows = 64;  // vocabulary rows per LM-head workgroup (one s
 // row's top-K.
 constexpr int kTileWords = 4;
 hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
+hipError_t launch_stochastic(const StochArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
 hipError_t launch_zero_i32(int32_t* p, size_t n, hipStream_t s);
 
 }  // namespace respec

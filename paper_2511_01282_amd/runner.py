@@ -54,7 +54,8 @@ def step_kwargs(w, params=None) -> dict:
                 max_nodes_in_batch=max(int(n_per.max()) if len(n_per) else 1, 1),
                 max_kv_len_in_batch=int(w.kv_len.max()) if len(w.kv_len) else 0,
                 kv_capacity=int(w.k_cache.shape[2]),
-                topk=p.topk, tau=p.tau, min_lookahead=p.min_lookahead, max_relaxed=p.max_relaxed)
+                topk=p.topk, tau=p.tau, min_lookahead=p.min_lookahead, max_relaxed=p.max_relaxed,
+                stochastic=getattr(p, "stochastic", 0), temperature=getattr(p, "temperature", 1.0))
 
 
 def run(w, *, plan=None, inputs=None, params=None, stop_after=binding.STOP_ALL, attn_out=True,

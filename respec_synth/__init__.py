@@ -178,6 +178,8 @@ class AcceptParams:
     tau: float = 3.0      # tolerance margin tau (Section 3.4)
     min_lookahead: int = 2  # m: greedy matches required after a relaxed token
     max_relaxed: int = 2    # Phi: number of relaxed attempts
+    stochastic: int = 0     # 1: speculative-sampling verification (Section 3.4, drafter outputs)
+    temperature: float = 1.0
 
 
 @dataclass

@@ -98,11 +98,11 @@ def _args(b, **over):
     a = b.Args()
     a.batch, a.total_nodes, a.max_nodes_in_batch, a.max_kv_len_in_batch = 1, 26, 26, 2048
     a.kv_capacity, a.stop_after = 2074, 0
-    a.accept = b.AcceptParams(8, 3.0, 2, 2)
+    a.accept = b.AcceptParams(8, 3.0, 2, 2, 0, 1.0)
     for f in b.INPUT_FIELDS + b.OUTPUT_FIELDS:
         setattr(a, f, FAKE)
     for k, v in over.items():
-        if k in ("topk", "tau", "min_lookahead", "max_relaxed"):
+        if k in ("topk", "tau", "min_lookahead", "max_relaxed", "stochastic", "temperature"):
             setattr(a.accept, k, v)
         else:
             setattr(a, k, v)
@@ -118,6 +118,10 @@ def _args(b, **over):
     (dict(hidden=None), 1), (dict(k_cache=None), 1), (dict(parent=None), 1), (dict(lm_head=None), 1),
     (dict(logits=None), 1), (dict(token=None), 1), (dict(flags=None), 1), (dict(seq_status=None), 1),
     (dict(hidden=FAKE + 8), 2), (dict(lm_head=FAKE + 4), 2), (dict(logits=FAKE + 4), 2),
+    # stochastic verification: mode, temperature, uniforms, draft distribution alignment
+    (dict(stochastic=2), 4), (dict(stochastic=1, temperature=0.0), 4), (dict(stochastic=1, temperature=-1.0), 4),
+    (dict(stochastic=1, temperature=float("inf")), 4), (dict(stochastic=1, temperature=float("nan")), 4),
+    (dict(stochastic=1, uniform=None), 1), (dict(stochastic=1, draft_prob=FAKE + 4), 2),
 ])
 def test_step_rejects_bad_arguments_before_launch(b, over, code):
     _, h = _create(b, _shape(b))

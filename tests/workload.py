@@ -169,3 +169,97 @@ def _exercise(w, z32, amax):
                 r = min(r, z32.shape[1] - 1)
                 w.token[j] = int(order[r])
                 steered.add(j)
+
+
+# ---------------------------------------------------------------------------
+# Stochastic verification inputs
+# ---------------------------------------------------------------------------
+
+STOCH_DRAW_MARGIN = 2e-4   # relative to the residual's total mass
+
+
+def _softmax_T(z, T):
+    e = np.exp((z - z.max()) / T)
+    return e / e.sum()
+
+
+def stochastic_inputs(case: Case, temperature: float, *, seed: int = 3, with_q: bool = True, q_noise: float = 0.5):
+    """Drafter distributions and uniforms for stochastic verification of ``case``.
+
+    q at node i is softmax((z_i + noise) / T), a drafter close to the target;
+    uniforms come from a seeded stream and are redrawn until every decision the
+    walk can take sits >= MARGIN from its threshold (acceptance tests) or
+    >= STOCH_DRAW_MARGIN of the residual mass from its bucket's edges (draws),
+    so that float32 and float64 arithmetic decide alike.  Returns (q, u).
+    """
+    w = case.w
+    z32 = case.z.astype(np.float32)
+    M, V = z32.shape
+    rng = np.random.default_rng(seed)
+    q = None
+    if with_q:
+        q = np.empty((M, V), np.float32)
+        for i in range(M):
+            q[i] = _softmax_T(z32[i].astype(np.float64) + rng.normal(0, q_noise, V), temperature).astype(np.float32)
+    u = rng.random((M, 2)).astype(np.float32)
+    B = len(w.node_off) - 1
+    for b in range(B):
+        lo, hi = int(w.node_off[b]), int(w.node_off[b + 1])
+        par = w.parent[lo:hi]
+        for li in range(hi - lo):
+            i = lo + li
+            r = _softmax_T(z32[i].astype(np.float64), temperature)
+            kids = [j for j in range(li + 1, hi - lo) if par[j] == li]
+            for j in kids:
+                t = int(w.token[lo + j])
+                model = q is not None and int(w.src[lo + j]) != synth.SRC_RETRIEVED
+                qk = q[i].astype(np.float64) if model else np.eye(1, V, t)[0]
+                a = min(1.0, r[t] / qk[t]) if qk[t] > 0 else (1.0 if r[t] > 0 else 0.0)
+                while abs(float(u[lo + j, 0]) - a) < MARGIN or (a >= 1.0 and u[lo + j, 0] > 1 - MARGIN):
+                    u[lo + j, 0] = np.float32(rng.random())
+                if float(u[lo + j, 0]) < a:
+                    break                       # accepted: this node never draws
+                d = np.maximum(r - qk, 0.0)
+                if d.sum() > 0:
+                    r = d / d.sum()
+            else:
+                c = np.cumsum(r)
+                tot = c[-1]
+                while True:
+                    thr = float(u[i, 1]) * tot
+                    v = int(np.searchsorted(c, thr, side="right"))
+                    lo_edge = c[v - 1] if v > 0 else 0.0
+                    if v < V and thr - lo_edge >= STOCH_DRAW_MARGIN * tot and c[v] - thr >= STOCH_DRAW_MARGIN * tot:
+                        break
+                    u[i, 1] = np.float32(rng.random())
+    return q, u
+
+
+def stochastic_expected(case: Case, q, u, temperature: float) -> dict:
+    """The oracle's stochastic verification of every sequence of ``case``."""
+    w = case.w
+    e = case.expected
+    z32 = case.z.astype(np.float32)
+    M = z32.shape[0]
+    B = len(w.node_off) - 1
+    D = w.shape.max_depth
+    out = dict(flags=e["flags"].copy(), sample=np.full(M, -1, np.int32), path=e["path"].copy(),
+               acc_len=e["acc_len"].copy(), bonus=e["bonus"].copy(), winner_leaf=e["winner_leaf"].copy(),
+               leaf_acc_len=e["leaf_acc_len"].copy())
+    for b in range(B):
+        lo, hi = int(w.node_off[b]), int(w.node_off[b + 1])
+        if int(e["seq_status"][b]) != 0:
+            continue
+        r = oracle.stochastic(w.parent[lo:hi], w.token[lo:hi], w.src[lo:hi], z32[lo:hi],
+                              None if q is None else q[lo:hi], u[lo:hi], temperature, D)
+        f = out["flags"][lo:hi] & np.uint8(~(oracle.FLAG_ON_PATH | 32) & 0xFF)
+        f |= (r["acc_bit"] * 32).astype(np.uint8)
+        f[r["path"][:r["acc_len"] + 1]] |= np.uint8(oracle.FLAG_ON_PATH)
+        out["flags"][lo:hi] = f
+        out["sample"][lo:hi] = r["sample"]
+        out["path"][b] = r["path"]
+        out["acc_len"][b] = r["acc_len"]
+        out["bonus"][b] = r["bonus"]
+        out["winner_leaf"][b] = r["winner_leaf"]
+        out["leaf_acc_len"][lo:hi] = r["leaf_acc_len"]
+    return out
