@@ -277,6 +277,43 @@ def main():
                        "bytes": nb["vocab"]},
         "step_events_us": avg["step"] * 1e3,
     }
+    # stochastic verification (speculative sampling, Section 3.4 for drafter outputs) on the
+    # same inputs: drafter distributions near the target's (softmax of the logits plus
+    # N(0, 0.5^2) noise) and seeded uniforms, made before the timed region
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    q = torch.softmax(out["logits"] + 0.5 * torch.randn(out["logits"].shape, generator=g, device=dev), dim=-1)
+    q = q.contiguous()
+    u = torch.rand((M, 2), generator=g, device=dev)
+    out_s = binding.alloc_outputs(total_nodes=M, batch=B, hidden=shp.hidden, vocab=shp.vocab,
+                                  topk_out=shp.topk_out, max_depth=shp.max_depth, device=dev, attn_out=False)
+    sets_s = [dict(x, draft_prob=q, uniform=u) for x in sets]
+    kw_s = dict(kw, stochastic=1, temperature=1.0)
+    for i in range(max(2, args.warmup // 4)):
+        plan.step(sets_s[i % R], out_s, stream=stream, **kw_s)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        plan.step(sets_s[i % R], out_s, stream=stream, **kw_s)
+    torch.cuda.synchronize()
+    wall_s = time.perf_counter() - t0
+    evs_s = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    for row in evs_s:
+        for e in row:
+            e.record(stream)
+    torch.cuda.synchronize()
+    for i in range(K):
+        plan.step(sets_s[i % R], out_s, stream=stream, stage_events=evs_s[i], **kw_s)
+    torch.cuda.synchronize()
+    stochastic = {
+        "steps_per_s": round(K / wall_s, 2), "us_per_step": round(wall_s * 1e6 / K, 2),
+        "vocab_pass_us": round(float(np.mean([r[2].elapsed_time(r[3]) for r in evs_s])) * 1e3, 3),
+        "mean_accepted": round(float(out_s["acc_len"].float().mean().item()), 3),
+        "what": "same step with speculative-sampling verification (temperature 1); the vocabulary "
+                "stage includes the sampling walk",
+    }
+    log(f"[bench] stochastic: {stochastic['us_per_step']:.1f} us/step, vocab stage {stochastic['vocab_pass_us']:.1f} us")
+
     dom = max(("attention", "lm_head", "vocab_pass"), key=lambda k: stages[k]["us"])
     achieved = stages[dom]["GB/s"]
     traffic = lmhead_traffic(cfg) if dom == "lm_head" else None
@@ -322,7 +359,7 @@ def main():
         "value": round(K / wall, 2), "unit": "steps/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if shp.dtype == "bf16" else "f32", "data": "synthetic", "config": wl,
-        "roofline": roofline, "cpu_baseline": cpu, "draft_host": draft_host,
+        "roofline": roofline, "cpu_baseline": cpu, "draft_host": draft_host, "stochastic": stochastic,
         "stages": {k: ({kk: round(vv, 3) for kk, vv in v.items()} if isinstance(v, dict) else round(v, 3))
                    for k, v in stages.items()},
         "device": torch.cuda.get_device_name(dev),

@@ -120,7 +120,8 @@ typedef struct {
   float tau;             /* tolerance margin, >= 0 (in nats = logit units)                 */
   int32_t min_lookahead; /* m: greedy matches required after a relaxed token, >= 0         */
   int32_t max_relaxed;   /* Phi: relaxed attempts per candidate chain, >= 0                */
-  int32_t stochastic;    /* 0: greedy strict / relaxed verification; 1: speculative sampling */
+  int32_t stochastic;    /* 0: greedy strict / relaxed verification; 1: speculative sampling
+                            (vocab <= 524288, else RESPEC_ERR_SHAPE)                    */
   float temperature;     /* T of stochastic verification, finite and > 0                   */
 } respec_accept_params;
 

@@ -193,6 +193,7 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
         q.max_relaxed < 0 || (q.stochastic != 0 && q.stochastic != 1))
       return RESPEC_ERR_PARAM;
     if (q.stochastic && (!(q.temperature > 0.f) || isinf(q.temperature))) return RESPEC_ERR_PARAM;
+    if (q.stochastic && s.vocab > kMaxStochVocab) return RESPEC_ERR_SHAPE;
   }
   const bool stochastic = full && a.accept.stochastic;
   hipStream_t st = static_cast<hipStream_t>(stream);

@@ -120,6 +120,7 @@ constexpr int kLmTileRows = 64;  // vocabulary rows per LM-head workgroup (one s
 constexpr int kTileWords = 4;
 hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
 hipError_t launch_stochastic(const StochArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
+constexpr int kMaxStochVocab = 256 * 2048;  // the draw's per-tile masses: 256 tiles of 2048 tokens
 hipError_t launch_zero_i32(int32_t* p, size_t n, hipStream_t s);
 
 }  // namespace respec

@@ -11,16 +11,23 @@
 // uniforms are inputs: u[j][0] decides child j, u[j][1] the residual draw at
 // node j (inverse CDF over the tokens in increasing order).
 //
-// One workgroup per node row i (after the vocabulary pass, which has written
-// the row's max logit and log-sum-exp):
-//   - the residual after k rejections is evaluated on the fly from z, the
-//     q row and the k normalisers, so a rejection costs one pass over the
-//     vocabulary (coalesced 16-byte loads, block-wide sum) and nothing is
-//     stored per token;
+// One workgroup of 512 threads per node row i (after the vocabulary pass,
+// which has written the row's max logit and log-sum-exp):
+//   - the residual keeps a closed form: after any sequence of rejections
+//     r(v) = [v not in X] * max(p(v) - c * q(v), 0) / N, where X holds the
+//     rejected retrieved tokens and c, N are scalars.  Rejecting a retrieved
+//     t adds t to X and divides by 1 - r(t) (the mass of every other token);
+//     rejecting a model draft sets c <- c + N and multiplies N by the sum of
+//     max(p - (c + N) q, 0) over the tokens outside X, one pass over the
+//     vocabulary.  So only model rejections and the draw read the row, and a
+//     token costs one exponential, one multiply-add and a max.  A pass walks
+//     tiles of 2048 tokens, one 16-byte group per thread per tile, with eight
+//     tiles' loads in flight per thread (a single workgroup's pass is
+//     latency-bound);
 //   - the children are tested until one passes; if none does, the residual is
-//     drawn: each thread sums its contiguous segment of tokens, a block scan
-//     gives the segment offsets, and the thread whose segment holds the
-//     threshold walks it again;
+//     drawn in two levels: the same kind of pass leaves each tile's mass in
+//     LDS, one wave scans the tile masses to find the tile that holds the
+//     threshold, and a block scan inside that tile finds the token;
 //   - the row hands its outcome (accepted child, or the draw) to the last row
 //     of its sequence (device-scope ticket), which walks the tree from the
 //     root along the accepted children and writes the path, the bonus token,
@@ -32,24 +39,28 @@
 namespace respec {
 namespace {
 
-constexpr int kST = 256;  // threads per row workgroup
-constexpr int kSW = kST / 64;
+constexpr int kST = 512;           // threads per row workgroup
+constexpr int kSW = kST / 64;      // waves
+constexpr int kTile = 4 * kST;     // tokens per tile: one group of 4 per thread
+constexpr int kUnroll = 8;         // tiles in flight per thread
+constexpr int kMaxTiles = 256;     // vocabularies up to 524288 tokens (checked on the host)
+static_assert(kMaxTiles * kTile == kMaxStochVocab, "host limit and LDS table agree");
 
 struct StochLds {
   int par[kMaxNodes];
   int tok[kMaxNodes];
   uint8_t src[kMaxNodes];
   int kid[kMaxNodes];       // children of the row (sequence-local), in node order
-  int ktok[kMaxNodes];
-  uint8_t kmodel[kMaxNodes];
-  float kinvz[kMaxNodes];   // 1 / normaliser of each rejected child's residual (0: residual kept)
+  int excl[kMaxNodes];      // X: rejected retrieved tokens
   uint64_t kids[2];
   float red[kSW];
-  float scan[kST];
-  int lastpos[kSW];
-  int b, n0, n, ok;
+  float tsum[kMaxTiles][kSW];  // residual mass per tile and wave (the draw)
+  int imin[kSW];
+  int b, ok;
   int ticket;
-  int sample;
+  int tile;                 // tile that holds the draw's threshold, -1 past the end
+  float tile_pre;           // residual mass before that tile
+  float thr;                // the draw's threshold (uniform times the residual mass)
   // the walk (last row of the sequence)
   int nxt[kMaxNodes];
   uint8_t has_child[kMaxNodes];
@@ -68,21 +79,77 @@ __device__ __forceinline__ float block_sum(float v, StochLds& sh, int lane, int 
   return s;
 }
 
-// Residual after nrej rejected children, at token v (z: logit, qv: the row's
-// draft probability of v or 0).
-__device__ __forceinline__ float residual(float z, float qv, int v, int nrej, const StochLds& sh, float m, float inv_t,
-                                          float inv_s) {
-  float r = __expf((z - m) * inv_t) * inv_s;
-  for (int k = 0; k < nrej; ++k) {
-    const float iz = sh.kinvz[k];
-    if (iz > 0.f) {
-      const float q = sh.kmodel[k] ? qv : (v == sh.ktok[k] ? 1.f : 0.f);
-      r = fmaxf(r - q, 0.f) * iz;
-    }
-  }
+__device__ __forceinline__ int block_min(int v, StochLds& sh, int lane, int wave) {
+  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
+  if (lane == 0) sh.imin[wave] = v;
+  __syncthreads();
+  int r = sh.imin[0];
+#pragma unroll
+  for (int w = 1; w < kSW; ++w) r = min(r, sh.imin[w]);
+  __syncthreads();
   return r;
 }
 
+// Four consecutive values of a row from token v (zeros past the end).  vec:
+// the vocabulary is a multiple of 4, so rows are 16-byte aligned.  The loads
+// are unconditional (clamped addresses, values masked afterwards): a load
+// under a branch would make the compiler wait for every earlier load first.
+template <bool Vec>
+__device__ __forceinline__ f32x4 load4(const float* row, int v, int V) {
+  if constexpr (Vec) {
+    const f32x4 x = *reinterpret_cast<const f32x4*>(row + min(v, V - 4));
+    const bool in = v < V;
+    return f32x4{in ? x.x : 0.f, in ? x.y : 0.f, in ? x.z : 0.f, in ? x.w : 0.f};
+  } else {
+    const float x0 = row[min(v, V - 1)], x1 = row[min(v + 1, V - 1)], x2 = row[min(v + 2, V - 1)],
+                x3 = row[min(v + 3, V - 1)];
+    return f32x4{v < V ? x0 : 0.f, v + 1 < V ? x1 : 0.f, v + 2 < V ? x2 : 0.f, v + 3 < V ? x3 : 0.f};
+  }
+}
+
+struct Row {
+  const float* z;
+  const float* q;   // null: no model draft rejected or tested yet (or no drafter input)
+  int V;
+  float m, inv_t, inv_s;
+};
+
+// p(v) = softmax(z / T)(v)
+__device__ __forceinline__ float target_p(const Row& r, float z) { return __expf((z - r.m) * r.inv_t) * r.inv_s; }
+
+__device__ __forceinline__ bool excluded(const StochLds& sh, int n_excl, int v) {
+  bool e = false;
+  for (int k = 0; k < n_excl; ++k) e = e || sh.excl[k] == v;
+  return e;
+}
+
+// One pass over the row: thread tid takes tokens 4 * (c * kST + tid) .. +3 of
+// every tile c; f(z4, q4, v, c) returns that group's contribution.
+template <bool Vec, typename F>
+__device__ __forceinline__ float row_pass(const Row& r, int tid, F f) {
+  const int n_tiles = (r.V + kTile - 1) / kTile;
+  float s = 0.f;
+  for (int c0 = 0; c0 < n_tiles; c0 += kUnroll) {
+    f32x4 z[kUnroll], q[kUnroll];
+    const float* qp = r.q ? r.q : r.z;  // (without a q row the loaded values are unused)
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int v = 4 * ((c0 + u) * kST + tid);
+      z[u] = load4<Vec>(r.z, v, r.V);
+      q[u] = load4<Vec>(qp, v, r.V);
+    }
+    if (!r.q)
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) q[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      if (c0 + u < n_tiles) s += f(z[u], q[u], 4 * ((c0 + u) * kST + tid), c0 + u);
+    }
+  }
+  return s;
+}
+
+template <bool Vec>
 __global__ __launch_bounds__(kST) void stochastic_kernel(StochArgs a) {
   __shared__ StochLds sh;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -124,149 +191,212 @@ __global__ __launch_bounds__(kST) void stochastic_kernel(StochArgs a) {
   __syncthreads();
   if (wave < 2) {
     const int j = tid;
-    const uint64_t m = __ballot(j < n && j > li && sh.par[j] == li);
-    if (lane == 0) sh.kids[wave] = m;
+    const uint64_t mk = __ballot(j < n && j > li && sh.par[j] == li);
+    if (lane == 0) sh.kids[wave] = mk;
   }
   __syncthreads();
-  int nk = 0;
-  {
-    uint64_t m0 = sh.kids[0], m1 = sh.kids[1];
-    if (tid == 0) {
-      while (m0) {
-        const int j = __builtin_ctzll(m0);
-        m0 &= m0 - 1;
-        sh.ktok[nk] = sh.tok[j];
-        sh.kmodel[nk] = a.draft_prob && sh.src[j] != RESPEC_SRC_RETRIEVED;
-        sh.kinvz[nk] = 0.f;
-        sh.kid[nk] = j;
-        ++nk;
+  const int nk = __popcll(sh.kids[0]) + __popcll(sh.kids[1]);
+  if (tid == 0) {
+    int c = 0;
+    for (int h = 0; h < 2; ++h)
+      for (uint64_t mk = sh.kids[h]; mk; mk &= mk - 1) {
+        const int j = 64 * h + __builtin_ctzll(mk);
+        sh.kid[c] = j;
+        ++c;
       }
-      while (m1) {
-        const int j = 64 + __builtin_ctzll(m1);
-        m1 &= m1 - 1;
-        sh.ktok[nk] = sh.tok[j];
-        sh.kmodel[nk] = a.draft_prob && sh.src[j] != RESPEC_SRC_RETRIEVED;
-        sh.kinvz[nk] = 0.f;
-        sh.kid[nk] = j;
-        ++nk;
-      }
-    }
-    nk = __popcll(sh.kids[0]) + __popcll(sh.kids[1]);
   }
   __syncthreads();
 
-  const float* zr = a.logits + (size_t)i * a.vocab;
-  const float* qr = a.draft_prob ? a.draft_prob + (size_t)i * a.vocab : nullptr;
-  const float m = a.max_logit[i];
-  const int V = a.vocab;
-  const bool vec = (V & 3) == 0;
+  Row row;
+  row.z = a.logits + (size_t)i * a.vocab;
+  row.q = nullptr;
+  row.V = a.vocab;
+  row.m = a.max_logit[i];
+  row.inv_t = a.inv_temp;
+  row.inv_s = 1.f;
+  const float* qrow = a.draft_prob ? a.draft_prob + (size_t)i * a.vocab : nullptr;
 
   // ---- p = softmax(z / T): the normaliser ----
-  float inv_s;
   if (a.unit_temp) {
-    inv_s = __expf(m - a.lse[i]);
+    row.inv_s = __expf(row.m - a.lse[i]);
   } else {
-    float s = 0.f;
-    if (vec) {
-      for (int v = 4 * tid; v < V; v += 4 * kST) {
-        const f32x4 z4 = *reinterpret_cast<const f32x4*>(zr + v);
-        s += __expf((z4.x - m) * a.inv_temp) + __expf((z4.y - m) * a.inv_temp) + __expf((z4.z - m) * a.inv_temp) +
-             __expf((z4.w - m) * a.inv_temp);
-      }
-    } else {
-      for (int v = tid; v < V; v += kST) s += __expf((zr[v] - m) * a.inv_temp);
-    }
-    inv_s = 1.f / block_sum(s, sh, lane, wave);
+    const float s = row_pass<Vec>(row, tid, [&](f32x4 z, f32x4, int v, int) {
+      float t = 0.f;
+      t += v < row.V ? __expf((z.x - row.m) * row.inv_t) : 0.f;
+      t += v + 1 < row.V ? __expf((z.y - row.m) * row.inv_t) : 0.f;
+      t += v + 2 < row.V ? __expf((z.z - row.m) * row.inv_t) : 0.f;
+      t += v + 3 < row.V ? __expf((z.w - row.m) * row.inv_t) : 0.f;
+      return t;
+    });
+    row.inv_s = 1.f / block_sum(s, sh, lane, wave);
   }
 
   // ---- the children, in node order, until one passes ----
-  int accepted = -1;
-  bool any_model = false;
+  // residual r(v) = [v not in X] * max(p(v) - c q(v), 0) * inv_n
+  int accepted = -1, n_excl = 0;
+  float c = 0.f, inv_n = 1.f;
   for (int k = 0; k < nk; ++k) {
-    const int t = sh.ktok[k];
-    const bool model = sh.kmodel[k];
-    any_model = any_model || model;
-    const float qt_row = qr ? qr[t] : 0.f;
-    const float rt = residual(zr[t], qt_row, t, k, sh, m, a.inv_temp, inv_s);
+    const int j = sh.kid[k];
+    const int t = sh.tok[j];
+    const bool model = qrow && sh.src[j] != RESPEC_SRC_RETRIEVED;
+    const float qt_row = qrow ? qrow[t] : 0.f;
+    const float rt = excluded(sh, n_excl, t) ? 0.f : fmaxf(target_p(row, row.z[t]) - c * qt_row, 0.f) * inv_n;
     const float qt = model ? qt_row : 1.f;
     const float acc = qt > 0.f ? fminf(rt / qt, 1.f) : (rt > 0.f ? 1.f : 0.f);
-    if (a.uniform[2 * (size_t)(n0 + sh.kid[k])] < acc) {
+    if (a.uniform[2 * (size_t)(n0 + j)] < acc) {
       accepted = k;
       break;
     }
-    // rejected: the normaliser of max(r - q_k, 0)
-    float s = 0.f;
-    const bool rd_q = qr && any_model;
-    if (vec) {
-      for (int v = 4 * tid; v < V; v += 4 * kST) {
-        const f32x4 z4 = *reinterpret_cast<const f32x4*>(zr + v);
-        const f32x4 q4 = rd_q ? *reinterpret_cast<const f32x4*>(qr + v) : f32x4{0.f, 0.f, 0.f, 0.f};
-        const float zz[4] = {z4.x, z4.y, z4.z, z4.w};
-        const float qq[4] = {q4.x, q4.y, q4.z, q4.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float r = residual(zz[e], qq[e], v + e, k, sh, m, a.inv_temp, inv_s);
-          const float q = model ? qq[e] : (v + e == t ? 1.f : 0.f);
-          s += fmaxf(r - q, 0.f);
-        }
+    if (!model) {
+      // max(r - onehot(t), 0) keeps every other token's mass: normaliser 1 - r(t)
+      const float zn = 1.f - rt;
+      if (zn > 0.f && rt > 0.f) {
+        if (tid == 0) sh.excl[n_excl] = t;
+        ++n_excl;
+        inv_n /= zn;
+        __syncthreads();
       }
-    } else {
-      for (int v = tid; v < V; v += kST) {
-        const float qv = rd_q ? qr[v] : 0.f;
-        const float r = residual(zr[v], qv, v, k, sh, m, a.inv_temp, inv_s);
-        const float q = model ? qv : (v == t ? 1.f : 0.f);
-        s += fmaxf(r - q, 0.f);
-      }
+      continue;
     }
-    const float z = block_sum(s, sh, lane, wave);
-    if (tid == 0) sh.kinvz[k] = z > 0.f ? 1.f / z : 0.f;
-    __syncthreads();
+    // a rejected model draft: sum of max(r - q, 0) = inv_n * sum over v not in X of max(p - (c + N) q, 0)
+    row.q = qrow;
+    const float c2 = c + 1.f / inv_n;
+    float part = row_pass<Vec>(row, tid, [&](f32x4 z, f32x4 q, int v, int) {
+      float x = 0.f;
+      x += v < row.V ? fmaxf(target_p(row, z.x) - c2 * q.x, 0.f) : 0.f;
+      x += v + 1 < row.V ? fmaxf(target_p(row, z.y) - c2 * q.y, 0.f) : 0.f;
+      x += v + 2 < row.V ? fmaxf(target_p(row, z.z) - c2 * q.z, 0.f) : 0.f;
+      x += v + 3 < row.V ? fmaxf(target_p(row, z.w) - c2 * q.w, 0.f) : 0.f;
+      return x;
+    });
+    for (int e = tid; e < n_excl; e += kST) {
+      const int te = sh.excl[e];
+      part -= fmaxf(target_p(row, row.z[te]) - c2 * qrow[te], 0.f);
+    }
+    const float zn = block_sum(part, sh, lane, wave) * inv_n;
+    if (zn > 0.f) {
+      c = c2;
+      inv_n /= zn;
+    }
   }
+  const float* q_draw = c > 0.f ? qrow : nullptr;  // q enters the residual only after a model rejection
+  row.q = q_draw;
 
   // ---- no child passed: draw from the residual ----
   int sample = -1;
   if (accepted < 0) {
-    const bool rd_q = qr && any_model;
-    const int seg = (V + kST - 1) / kST;
-    const int v0 = tid * seg, v1 = min(V, v0 + seg);
-    float part = 0.f;
-    int last = -1;
-    for (int v = v0; v < v1; ++v) {
-      const float r = residual(zr[v], rd_q ? qr[v] : 0.f, v, nk, sh, m, a.inv_temp, inv_s);
-      part += r;
-      last = r > 0.f ? v : last;
-    }
-    // block exclusive scan of the segment sums (thread order = token order)
-    sh.scan[tid] = part;
-    const int lmax = wave_max((float)last);
-    if (lane == 0) sh.lastpos[wave] = lmax;
-    if (tid == 0) sh.sample = -1;
+    const int n_tiles = (row.V + kTile - 1) / kTile;
+    // level 1: the mass of max(p - c q, 0) in every tile (and wave), the
+    // rejected retrieved tokens taken out afterwards (the common scale inv_n
+    // does not change where the threshold falls)
+    row_pass<Vec>(row, tid, [&](f32x4 z, f32x4 q, int v, int tile) {
+      float x = 0.f;
+      x += v < row.V ? fmaxf(target_p(row, z.x) - c * q.x, 0.f) : 0.f;
+      x += v + 1 < row.V ? fmaxf(target_p(row, z.y) - c * q.y, 0.f) : 0.f;
+      x += v + 2 < row.V ? fmaxf(target_p(row, z.z) - c * q.z, 0.f) : 0.f;
+      x += v + 3 < row.V ? fmaxf(target_p(row, z.w) - c * q.w, 0.f) : 0.f;
+      x = wave_sum(x);
+      if (lane == 0) sh.tsum[tile][wave] = x;
+      return 0.f;
+    });
     __syncthreads();
-    float pre = 0.f, total = 0.f;
-    for (int u = 0; u < kST; ++u) {
-      const float x = sh.scan[u];
-      pre += u < tid ? x : 0.f;
-      total += x;
+    for (int e = tid; e < n_excl; e += kST) {
+      const int te = sh.excl[e];
+      const float x = fmaxf(target_p(row, row.z[te]) - c * (q_draw ? q_draw[te] : 0.f), 0.f);
+      atomicAdd(&sh.tsum[te / kTile][((te % kTile) / 4) / 64], -x);
     }
-    const float thr = a.uniform[2 * (size_t)i + 1] * total;
-    if (part > 0.f && pre <= thr && thr < pre + part) {
-      float s = 0.f;
-      for (int v = v0; v < v1; ++v) {
-        s += residual(zr[v], rd_q ? qr[v] : 0.f, v, nk, sh, m, a.inv_temp, inv_s);
-        if (pre + s > thr) {
-          sh.sample = v;
-          break;
+    __syncthreads();
+    const float u_draw = a.uniform[2 * (size_t)i + 1];
+    if (wave == 0) {
+      // lane l owns tiles 4l .. 4l+3; tile mass = its waves' sums in wave order
+      float tm[4], ls = 0.f;
+      int last_tile = -1;
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const int tc = 4 * lane + h;
+        float x = 0.f;
+        if (tc < n_tiles)
+#pragma unroll
+          for (int w = 0; w < kSW; ++w) x += sh.tsum[tc][w];
+        x = fmaxf(x, 0.f);
+        tm[h] = x;
+        ls += x;
+        last_tile = x > 0.f ? tc : last_tile;
+      }
+      float incl = ls;
+      for (int o = 1; o < 64; o <<= 1) {
+        const float y = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += y;
+      }
+      float excl = __shfl_up(incl, 1, 64);
+      if (lane == 0) excl = 0.f;
+      const float total = __shfl(incl, 63, 64);
+      const float thr = u_draw * total;
+      int tile = kMaxTiles;
+      float pre = excl;
+      if (excl <= thr && thr < incl) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          if (tile == kMaxTiles && tm[h] > 0.f && thr < pre + tm[h]) tile = 4 * lane + h;
+          if (tile == kMaxTiles) pre += tm[h];
         }
+      }
+      // the first lane that found a tile; rounding may leave none: then the
+      // last tile with mass, searched for its last token with mass
+      int best = tile;
+      for (int o = 32; o > 0; o >>= 1) best = min(best, __shfl_xor(best, o, 64));
+      int lt = last_tile;
+      for (int o = 32; o > 0; o >>= 1) lt = max(lt, __shfl_xor(lt, o, 64));
+      const int src_lane = best < kMaxTiles ? best / 4 : 0;
+      const float best_pre = __shfl(pre, src_lane, 64);
+      if (lane == 0) {
+        sh.tile = best < kMaxTiles ? best : max(lt, 0);
+        sh.tile_pre = best < kMaxTiles ? best_pre : 0.f;
+        sh.thr = best < kMaxTiles ? thr : __builtin_inff();
       }
     }
     __syncthreads();
-    sample = sh.sample;
-    if (sample < 0) {  // rounding put the threshold past the last segment: the last token with mass
-      int lp = -1;
+    const int tile = sh.tile;
+    const float thr = sh.thr;
+    // level 2: the token in the tile whose cumulative mass first exceeds the threshold
+    const int v = 4 * (tile * kST + tid);
+    const f32x4 z = load4<Vec>(row.z, v, row.V);
+    f32x4 q = load4<Vec>(q_draw ? q_draw : row.z, v, row.V);
+    if (!q_draw) q = f32x4{0.f, 0.f, 0.f, 0.f};
+    const float zz[4] = {z.x, z.y, z.z, z.w};
+    const float qq[4] = {q.x, q.y, q.z, q.w};
+    float xs[4], own = 0.f;
+    int tile_last = -1;
 #pragma unroll
-      for (int w = 0; w < kSW; ++w) lp = max(lp, sh.lastpos[w]);
-      sample = max(lp, 0);
+    for (int e = 0; e < 4; ++e) {
+      const bool in = v + e < row.V && !excluded(sh, n_excl, v + e);
+      xs[e] = in ? fmaxf(target_p(row, zz[e]) - c * qq[e], 0.f) : 0.f;
+      own += xs[e];
+      tile_last = xs[e] > 0.f ? v + e : tile_last;
     }
+    float incl = own;
+    for (int o = 1; o < 64; o <<= 1) {
+      const float y = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += y;
+    }
+    if (lane == 63) sh.red[wave] = incl;
+    __syncthreads();
+    float base = sh.tile_pre;
+    for (int w = 0; w < wave; ++w) base += sh.red[w];
+    float ex = __shfl_up(incl, 1, 64);
+    if (lane == 0) ex = 0.f;
+    base += ex;
+    int found = 0x7fffffff;
+    float cum = base;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      cum += xs[e];
+      if (found == 0x7fffffff && xs[e] > 0.f && cum > thr) found = v + e;
+    }
+    __syncthreads();
+    const int first = block_min(found, sh, lane, wave);
+    const int tl = -block_min(-tile_last, sh, lane, wave);
+    sample = max(first != 0x7fffffff ? first : tl, 0);
   }
 
   // ---- hand-off and the sequence's completion ticket ----
@@ -343,7 +473,10 @@ __global__ __launch_bounds__(kST) void stochastic_kernel(StochArgs a) {
 }  // namespace
 
 hipError_t launch_stochastic(const StochArgs& a, hipStream_t s, hipEvent_t ev_stop) {
-  return launch_k(stochastic_kernel, dim3(a.total_nodes), dim3(kST), 0, s, nullptr, ev_stop, a);
+  // vocabularies that are a multiple of 4 have 16-byte aligned rows
+  if ((a.vocab & 3) == 0)
+    return launch_k(stochastic_kernel<true>, dim3(a.total_nodes), dim3(kST), 0, s, nullptr, ev_stop, a);
+  return launch_k(stochastic_kernel<false>, dim3(a.total_nodes), dim3(kST), 0, s, nullptr, ev_stop, a);
 }
 
 }  // namespace respec
