@@ -66,10 +66,24 @@ def stage_bytes(w, M, es):
     return dict(attn=attn, lm=lm, vocab=vocab, attn_flops=attn_flops, lm_flops=lm_flops)
 
 
+def lmhead_source_hash():
+    """Hash of what the LM-head kernel is compiled from: lmhead.hip, common.hpp and the
+    LmArgs struct of kernels.hpp (the other launch declarations there do not change it)."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2511_01282_amd", "csrc")
+    h = hashlib.sha256()
+    for f in ("lmhead.hip", "common.hpp"):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    text = open(os.path.join(csrc, "kernels.hpp")).read()
+    a = text.index("struct LmArgs {")
+    h.update(text[a:text.index("};", a) + 2].encode())
+    return h.hexdigest()[:16]
+
+
 def lmhead_traffic(cfg):
     """HBM bytes per LM-head launch from the committed counter profile of the 7B-shaped
     workload, or None when the kernel sources changed since the counters were taken."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", "lmhead_7b_26node_hbm_traffic.txt")
     if cfg != 1 or not os.path.exists(path):
         return None
@@ -78,11 +92,7 @@ def lmhead_traffic(cfg):
         parts = line.split()
         if len(parts) >= 2 and parts[0] in ("lmhead_traffic_bytes", "lmhead_source_sha256_16"):
             fields[parts[0]] = parts[1]
-    h = hashlib.sha256()
-    for f in ("lmhead.hip", "common.hpp", "kernels.hpp"):
-        with open(os.path.join(ROOT, "paper_2511_01282_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    if fields.get("lmhead_source_sha256_16") != h.hexdigest()[:16]:
+    if fields.get("lmhead_source_sha256_16") != lmhead_source_hash():
         return None
     return int(fields["lmhead_traffic_bytes"])
 
