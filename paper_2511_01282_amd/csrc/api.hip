@@ -23,6 +23,7 @@ struct respec_verify_plan {
   int attn_stages;        // ring slots of the shared-tile kernel
   int attn_kg;            // key groups of the shared-tile kernel
   int attn_wg_target;     // workgroups the splits aim for
+  int flat_pieces;        // ragged batches (register path): pieces of each head's KV tiles
   size_t attn_lds;
   // vocabulary statistics: tiles of the LM head and the top-K width (8 or 16)
   int ko, n_vtiles;
@@ -141,13 +142,16 @@ respec_status respec_verify_create(const respec_verify_shape* shape, respec_veri
   }
   const int per_split = s.n_kv_heads * p->n_rowblk;
   p->nsplit_cap = clampi(p->attn_wg_target / per_split, 1, cdiv(t_cap, kKvTile));
+  // one piece per CU (two per CU measured slower on an 8-sequence ragged batch: 158 against 144 us)
+  p->flat_pieces = p->attn_shared ? 0 : clampi(p->attn_wg_target / per_split, 1, 64);
+  const int slots = p->nsplit_cap > p->flat_pieces ? p->nsplit_cap : p->flat_pieces;
 
   p->ko = s.topk_out <= 8 ? 8 : 16;
   p->n_vtiles = cdiv(s.vocab, kLmTileRows);
 
   // workspace
   const size_t mcap = (size_t)s.max_batch * s.max_nodes;
-  const size_t prow = (size_t)s.max_batch * s.n_kv_heads * p->n_rowblk * p->nsplit_cap * p->rows_per_wg;
+  const size_t prow = (size_t)s.max_batch * s.n_kv_heads * p->n_rowblk * slots * p->rows_per_wg;
   size_t off = 0;
   p->off_po = off; off = align256(off + prow * s.head_dim * 4);
   p->off_pm = off; off = align256(off + prow * 4);
@@ -255,12 +259,23 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   const int target = clampi(plan->attn_wg_target / per_split, 1, plan->nsplit_cap);
   at.chunk = cdiv(cdiv(t_max, target), kKvTile) * kKvTile;
   at.nsplit = cdiv(t_max, at.chunk);
+  at.flat = 0;
+  at.batch = a.batch;
+  // Ragged batches on the register path: each head's KV tiles over every sequence are cut
+  // into equal pieces, one workgroup each, so that the longest sequence does not finish
+  // alone (per-sequence splits leave every other workgroup idle at the end).
+  const bool flat = !plan->attn_shared && a.batch > 1 && a.batch <= 64;
+  if (flat) {
+    at.flat = plan->flat_pieces;
+    at.nsplit = at.flat;
+    at.chunk = 0;
+  }
   at.n_rowblk = plan->n_rowblk;
   at.rows_per_wg = plan->rows_per_wg;
   at.wr = plan->wr;
   at.wk = plan->wk;
   at.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.head_dim));
-  dim3 agrid(at.nsplit, s.n_kv_heads * plan->n_rowblk, a.batch);
+  dim3 agrid(at.nsplit, s.n_kv_heads * plan->n_rowblk, flat ? 1 : a.batch);
   const hipError_t ae =
       plan->attn_shared
           ? launch_tree_attn_shared(s.head_dim, plan->nb, plan->attn_stages, plan->attn_kg, agrid, plan->attn_threads,

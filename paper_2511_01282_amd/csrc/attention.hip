@@ -481,32 +481,65 @@ __device__ __forceinline__ void ancestor_bits(const int (&qnode)[NB], int p_lo, 
   }
 }
 
+// Rows of sequence b's KV range (prefix + tree); invalid device data degrades
+// to an empty sequence.  The merge computes the same, so both agree on the
+// flat partition.
+struct SeqRows {
+  int node0, n_nodes, L;
+};
+__device__ __forceinline__ SeqRows seq_rows(const AttnArgs& a, int b) {
+  const int node0 = a.node_off[b], node1 = a.node_off[b + 1];
+  int n_nodes = node1 - node0;
+  if (node0 < 0 || node1 > a.total_nodes || n_nodes < 1 || n_nodes > a.max_nodes) n_nodes = 0;
+  int L = a.kv_len[b];
+  L = max(0, min(L, a.kv_cap - n_nodes));
+  return SeqRows{node0, n_nodes, n_nodes > 0 ? L : 0};
+}
+
+// Flat partition of a head's KV tiles over the sequences of the batch (one
+// wave; lane l describes sequence l < batch <= 64): tiles of each sequence,
+// their exclusive prefix and the total.
+struct FlatTiles {
+  int tiles, pre, total;
+};
+__device__ __forceinline__ FlatTiles flat_tiles(const AttnArgs& a, int lane) {
+  int nt = 0;
+  if (lane < a.batch) {
+    const SeqRows sr = seq_rows(a, lane);
+    nt = sr.n_nodes > 0 ? (sr.L + sr.n_nodes + kKvTile - 1) / kKvTile : 0;
+  }
+  int incl = nt;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += y;
+  }
+  return FlatTiles{nt, incl - nt, __shfl(incl, 63, 64)};
+}
+// The piece (of P over `total` tiles, boundaries floor(p * total / P)) that holds tile x.
+__device__ __forceinline__ int flat_piece(int x, int P, int total) {
+  return (int)(((long long)(x + 1) * P - 1) / total);
+}
+
+// One segment of work: KV rows [kv_lo, min(kv_hi, t_rows)) of sequence b, KV
+// head g, row block rb, written to partial slot `slot`.
 template <typename T, int D, int NB>
-__global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
+__device__ __forceinline__ void attn_segment(const AttnArgs& a, unsigned char* s_work, int b, int g, int rb,
+                                             int kv_lo, int kv_hi_req, int slot) {
   constexpr int ES = Elem<T>::kBytes;
   constexpr int KCH = D * ES / 64;     // 64-byte K-chunks per head row
   constexpr int DB = D / 16;           // 16-wide output blocks along D
   constexpr int VTS = kKvTile + kVtPad;  // elements per transposed-V row (float32 path)
   constexpr int RB = 16 * NB;          // query rows per wave
 
-  extern __shared__ __align__(16) unsigned char smem[];
-  unsigned char* s_work = smem;
-
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar branches below
   const int lr = lane & 15, lg = lane >> 4;
   const int nwaves = blockDim.x >> 6;
   const int wr = wave % a.wr, wk = wave / a.wr;
-  const int b = blockIdx.z;
-  const int g = blockIdx.y / a.n_rowblk, rb = blockIdx.y % a.n_rowblk;
-  const int split = blockIdx.x;
+  const int split = slot;
 
-  // Sequence bounds; invalid device data degrades to an empty sequence.
-  const int node0 = a.node_off[b], node1 = a.node_off[b + 1];
-  int n_nodes = node1 - node0;
-  if (node0 < 0 || node1 > a.total_nodes || n_nodes < 1 || n_nodes > a.max_nodes) n_nodes = 0;
-  int L = a.kv_len[b];
-  L = max(0, min(L, a.kv_cap - n_nodes));
+  const SeqRows sr = seq_rows(a, b);
+  const int node0 = sr.node0, n_nodes = sr.n_nodes, L = sr.L;
   const int R = n_nodes * a.group;
   const int row_wg = rb * a.rows_per_wg;
   if (row_wg >= R) return;  // uniform over every split of this row block
@@ -515,8 +548,7 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
   const char* kbase = reinterpret_cast<const char*>(a.k_cache) + head_row0 * D * ES;
   const char* vbase = reinterpret_cast<const char*>(a.v_cache) + head_row0 * D * ES;
   const int t_rows = L + n_nodes;
-  const int kv_lo = split * a.chunk;
-  const int kv_hi = min(kv_lo + a.chunk, t_rows);
+  const int kv_hi = min(kv_hi_req, t_rows);
   const int t_first = kv_lo + wk * kKvTile, t_step = kKvTile * a.wk;
   const int n_tiles = t_first < kv_hi ? (kv_hi - t_first + t_step - 1) / t_step : 0;
 
@@ -697,6 +729,38 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
       }
       *reinterpret_cast<f32x4*>(a.part_o + (pbase + rl) * D + d) = acc;
     }
+  }
+}
+
+template <typename T, int D, int NB, bool Flat>
+__global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int g = blockIdx.y / a.n_rowblk, rb = blockIdx.y % a.n_rowblk;
+  if constexpr (!Flat) {
+    attn_segment<T, D, NB>(a, smem, blockIdx.z, g, rb, blockIdx.x * a.chunk, blockIdx.x * a.chunk + a.chunk,
+                           blockIdx.x);
+    return;
+  }
+  // Flat partition (ragged batches): piece p of this head's tiles over every
+  // sequence, so that every workgroup streams the same number of KV tiles
+  // whatever the lengths; a piece runs one segment per sequence it touches.
+  const int lane = threadIdx.x & 63;
+  const FlatTiles ft = flat_tiles(a, lane);
+  const int P = a.flat, p = blockIdx.x;
+  if (ft.total == 0) return;
+  const int T0 = (int)((long long)p * ft.total / P), T1 = (int)((long long)(p + 1) * ft.total / P);
+  const bool touches = lane < a.batch && ft.tiles > 0 && ft.pre < T1 && ft.pre + ft.tiles > T0;
+  uint64_t seqs = __ballot(touches);
+  bool first = true;
+  while (seqs) {
+    const int b = __builtin_ctzll(seqs);
+    seqs &= seqs - 1;
+    const int pre = __shfl(ft.pre, b, 64), nt = __shfl(ft.tiles, b, 64);
+    const int lo = max(T0, pre) - pre, hi = min(T1, pre + nt) - pre;
+    const int slot = p - flat_piece(pre, P, ft.total);
+    if (!first) __syncthreads();  // the previous segment's merge is done with the LDS
+    first = false;
+    attn_segment<T, D, NB>(a, smem, b, g, rb, lo * kKvTile, hi * kKvTile, slot);
   }
 }
 
@@ -1001,6 +1065,13 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   const int row_wg = rb * a.rows_per_wg;
   const int rl = blockIdx.x * kRows + (int)threadIdx.x / D4;  // row within the row block
   const int d = ((int)threadIdx.x % D4) * 4;
+  // partials of this sequence: every split, or (flat partition) the pieces its tiles span
+  int nsp = a.nsplit;
+  if (a.flat) {
+    const FlatTiles ft = flat_tiles(a, (int)threadIdx.x & 63);
+    const int pre = __shfl(ft.pre, b, 64), nt = __shfl(ft.tiles, b, 64);
+    nsp = nt > 0 ? flat_piece(pre + nt - 1, a.flat, ft.total) - flat_piece(pre, a.flat, ft.total) + 1 : 0;
+  }
   if (rl >= a.rows_per_wg || row_wg + rl >= R) return;
   const size_t sbase = (size_t)bgr * a.nsplit * a.rows_per_wg + rl;
   const size_t sstride = (size_t)a.rows_per_wg;
@@ -1015,13 +1086,13 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 
   float M = kNegInf, Ls = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int sp0 = 0; sp0 < a.nsplit; sp0 += kBatch) {
+  for (int sp0 = 0; sp0 < nsp; sp0 += kBatch) {
     float mv[kBatch], lv[kBatch];
     f32x4 ov[kBatch];
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const int sp = sp0 + u;
-      const bool ok = sp < a.nsplit;
+      const bool ok = sp < nsp;
       const size_t pr = sbase + (size_t)(ok ? sp : 0) * sstride;
       mv[u] = ok ? a.part_m[pr] : kNegInf;
       lv[u] = ok ? a.part_l[pr] : 0.f;
@@ -1052,22 +1123,37 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 template <typename T, int D>
 static hipError_t launch_nb(int nb, dim3 grid, int threads, size_t lds, const AttnArgs& a, hipStream_t s,
                             hipEvent_t ev_start) {
+  const bool flat = a.flat > 0;
   switch (nb) {
-    case 1: return launch_k(tree_attn_kernel<T, D, 1>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
-    case 2: return launch_k(tree_attn_kernel<T, D, 2>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
+    case 1:
+      return flat ? launch_k(tree_attn_kernel<T, D, 1, true>, grid, dim3(threads), lds, s, ev_start, nullptr, a)
+                  : launch_k(tree_attn_kernel<T, D, 1, false>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
+    case 2:
+      return flat ? launch_k(tree_attn_kernel<T, D, 2, true>, grid, dim3(threads), lds, s, ev_start, nullptr, a)
+                  : launch_k(tree_attn_kernel<T, D, 2, false>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <typename T, int D>
 static hipError_t set_lds_nb(int nb, size_t lds) {
-  const void* f = nullptr;
+  const void* f[2] = {nullptr, nullptr};
   switch (nb) {
-    case 1: f = reinterpret_cast<const void*>(&tree_attn_kernel<T, D, 1>); break;
-    case 2: f = reinterpret_cast<const void*>(&tree_attn_kernel<T, D, 2>); break;
+    case 1:
+      f[0] = reinterpret_cast<const void*>(&tree_attn_kernel<T, D, 1, false>);
+      f[1] = reinterpret_cast<const void*>(&tree_attn_kernel<T, D, 1, true>);
+      break;
+    case 2:
+      f[0] = reinterpret_cast<const void*>(&tree_attn_kernel<T, D, 2, false>);
+      f[1] = reinterpret_cast<const void*>(&tree_attn_kernel<T, D, 2, true>);
+      break;
     default: return hipErrorInvalidValue;
   }
-  return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  for (const void* k : f) {
+    const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int threads, size_t lds,

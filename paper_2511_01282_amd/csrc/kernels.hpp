@@ -28,6 +28,11 @@ struct AttnArgs {
   int32_t total_nodes, hidden_size, n_kv_heads, group, kv_cap, max_nodes;
   int32_t nsplit, chunk, n_rowblk, rows_per_wg, wr, wk;
   float scale_log2;        // log2(e) / sqrt(D)
+  // flat > 0 (register path, 2-64 sequences): blockIdx.x is one of `flat` equal pieces of
+  // the KV tiles of every sequence of its head (partial slots per sequence, nsplit = flat);
+  // 0: blockIdx.x is a split of `chunk` rows of sequence blockIdx.z
+  int32_t flat;
+  int32_t batch;
 };
 
 struct LmArgs {

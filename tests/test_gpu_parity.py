@@ -110,6 +110,11 @@ EDGE = {
     "f32-40-nodes": ("f32", 4, 4, 64, [[-1] + [j // 2 for j in range(0, 39)]], [100]),
     "f32-61-nodes": ("f32", 4, 4, 64, [[-1] + [max(0, j - 3) for j in range(1, 61)]], [77]),
     "bf16-56-nodes": ("bf16", 4, 2, 128, [[-1] + [j // 3 for j in range(0, 55)]], [64]),
+    # ragged batches on the register path (flat partition of each head's KV tiles)
+    # (the cache capacity covers the longest prefix plus the largest tree, as the ABI requires)
+    "f32-ragged": ("f32", 4, 4, 64, [[-1, 0, 1], [-1] + list(range(0, 20)), [-1, 0, 0, 0, 1]], [300, 1000, 17]),
+    "bf16-ragged-mha": ("bf16", 4, 4, 128, [[-1, 0, 1, 1], [-1] + list(range(0, 9)), [-1], [-1, 0, 0, 2, 3, 3]],
+                        [900, 3000, 40, 250]),
 }
 
 
