@@ -51,7 +51,9 @@ struct StochLds {
   int tok[kMaxNodes];
   uint8_t src[kMaxNodes];
   int kid[kMaxNodes];       // children of the row (sequence-local), in node order
-  int excl[kMaxNodes];      // X: rejected retrieved tokens
+  float kz[kMaxNodes];      // z_i[t] and q_i[t] of each child's token (requested together up front)
+  float kq[kMaxNodes];
+  int excl[kMaxNodes];      // X: rejected retrieved tokens (as child indices)
   uint64_t kids[2];
   float red[kSW];
   float tsum[kMaxTiles][kSW];  // residual mass per tile and wave (the draw)
@@ -119,7 +121,7 @@ __device__ __forceinline__ float target_p(const Row& r, float z) { return __expf
 
 __device__ __forceinline__ bool excluded(const StochLds& sh, int n_excl, int v) {
   bool e = false;
-  for (int k = 0; k < n_excl; ++k) e = e || sh.excl[k] == v;
+  for (int k = 0; k < n_excl; ++k) e = e || sh.tok[sh.kid[sh.excl[k]]] == v;
   return e;
 }
 
@@ -215,6 +217,13 @@ __global__ __launch_bounds__(kST) void stochastic_kernel(StochArgs a) {
   row.inv_t = a.inv_temp;
   row.inv_s = 1.f;
   const float* qrow = a.draft_prob ? a.draft_prob + (size_t)i * a.vocab : nullptr;
+  // every child's z and q at its token, in one round trip (the tests need nothing else per child)
+  for (int k = tid; k < nk; k += kST) {
+    const int t = sh.tok[sh.kid[k]];
+    sh.kz[k] = row.z[t];
+    sh.kq[k] = qrow ? qrow[t] : 0.f;
+  }
+  __syncthreads();
 
   // ---- p = softmax(z / T): the normaliser ----
   if (a.unit_temp) {
@@ -239,8 +248,8 @@ __global__ __launch_bounds__(kST) void stochastic_kernel(StochArgs a) {
     const int j = sh.kid[k];
     const int t = sh.tok[j];
     const bool model = qrow && sh.src[j] != RESPEC_SRC_RETRIEVED;
-    const float qt_row = qrow ? qrow[t] : 0.f;
-    const float rt = excluded(sh, n_excl, t) ? 0.f : fmaxf(target_p(row, row.z[t]) - c * qt_row, 0.f) * inv_n;
+    const float qt_row = sh.kq[k];
+    const float rt = excluded(sh, n_excl, t) ? 0.f : fmaxf(target_p(row, sh.kz[k]) - c * qt_row, 0.f) * inv_n;
     const float qt = model ? qt_row : 1.f;
     const float acc = qt > 0.f ? fminf(rt / qt, 1.f) : (rt > 0.f ? 1.f : 0.f);
     if (a.uniform[2 * (size_t)(n0 + j)] < acc) {
@@ -251,7 +260,7 @@ __global__ __launch_bounds__(kST) void stochastic_kernel(StochArgs a) {
       // max(r - onehot(t), 0) keeps every other token's mass: normaliser 1 - r(t)
       const float zn = 1.f - rt;
       if (zn > 0.f && rt > 0.f) {
-        if (tid == 0) sh.excl[n_excl] = t;
+        if (tid == 0) sh.excl[n_excl] = k;
         ++n_excl;
         inv_n /= zn;
         __syncthreads();
@@ -270,8 +279,8 @@ __global__ __launch_bounds__(kST) void stochastic_kernel(StochArgs a) {
       return x;
     });
     for (int e = tid; e < n_excl; e += kST) {
-      const int te = sh.excl[e];
-      part -= fmaxf(target_p(row, row.z[te]) - c2 * qrow[te], 0.f);
+      const int ke = sh.excl[e];
+      part -= fmaxf(target_p(row, sh.kz[ke]) - c2 * sh.kq[ke], 0.f);
     }
     const float zn = block_sum(part, sh, lane, wave) * inv_n;
     if (zn > 0.f) {
@@ -301,8 +310,9 @@ __global__ __launch_bounds__(kST) void stochastic_kernel(StochArgs a) {
     });
     __syncthreads();
     for (int e = tid; e < n_excl; e += kST) {
-      const int te = sh.excl[e];
-      const float x = fmaxf(target_p(row, row.z[te]) - c * (q_draw ? q_draw[te] : 0.f), 0.f);
+      const int ke = sh.excl[e];
+      const int te = sh.tok[sh.kid[ke]];
+      const float x = fmaxf(target_p(row, sh.kz[ke]) - c * (q_draw ? sh.kq[ke] : 0.f), 0.f);
       atomicAdd(&sh.tsum[te / kTile][((te % kTile) / 4) / 64], -x);
     }
     __syncthreads();
