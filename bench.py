@@ -286,6 +286,10 @@ def main():
         "vocab_pass": {"us": avg["vocab"] * 1e3, "GB/s": nb["vocab"] / (avg["vocab"] * 1e-3) / 1e9,
                        "bytes": nb["vocab"]},
         "step_events_us": avg["step"] * 1e3,
+        # distribution of the event-timed steps (attention start to vocabulary-pass end)
+        "step_us_p10": float(np.percentile(st["step"], 10)) * 1e3,
+        "step_us_p50": float(np.percentile(st["step"], 50)) * 1e3,
+        "step_us_p90": float(np.percentile(st["step"], 90)) * 1e3,
     }
     # stochastic verification (speculative sampling, Section 3.4 for drafter outputs) on the
     # same inputs: drafter distributions near the target's (softmax of the logits plus
@@ -330,8 +334,14 @@ def main():
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic}
     if dom == "lm_head":
+        # the matrix-core view of the same kernel: its fraction of the dense peak, and of the
+        # attainable roofline min(peak, arithmetic intensity x HBM peak) at this token count
         peak_tf = BF16_PEAK_TFLOPS if shp.dtype == "bf16" else FP32_PEAK_TFLOPS
+        ai = nb["lm_flops"] / nb["lm"]
+        attainable = min(peak_tf, ai * HBM_PEAK_GBS / 1e3)
         roofline["mfma_frac"] = round(stages["lm_head"]["TFLOP/s"] / peak_tf, 4)
+        roofline["attainable_tflops"] = round(attainable, 1)
+        roofline["frac_of_attainable"] = round(stages["lm_head"]["TFLOP/s"] / attainable, 4)
     log(f"[bench] {ms_step * 1e3:.1f} us/step; stages " +
         ", ".join(f"{k} {stages[k]['us']:.1f} us" for k in ("attention", "lm_head", "vocab_pass")))
 
