@@ -842,8 +842,26 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int grp = KG > 1 ? __builtin_amdgcn_readfirstlane(wave / a.wr) : 0;  // key group
-  const int rw = wave - grp * a.wr;                                            // row wave
+  // Roles: key group grp, row wave rw.  Waves w and w + 4 share a SIMD.  With two key groups
+  // the last row wave of each group holds the fewest live rows (65 rows: blocks 2, 2 and 1),
+  // so those two roles go to waves 0 and 1, whose SIMDs also carry waves 4 and 5: no SIMD then
+  // holds two full row waves of a three-wave group (65 rows: at most 3 blocks per SIMD, not 4).
+  int grp = 0, rw = wave;
+  if constexpr (KG > 1) {
+    if (a.wr == 1) {
+      grp = wave;
+      rw = 0;
+    } else if (wave < 2) {
+      grp = wave;
+      rw = a.wr - 1;
+    } else {
+      const int j = wave - 2;
+      grp = j / (a.wr - 1);
+      rw = j - grp * (a.wr - 1);
+    }
+    grp = __builtin_amdgcn_readfirstlane(grp);
+    rw = __builtin_amdgcn_readfirstlane(rw);
+  }
   const int lr = lane & 15, lg = lane >> 4;
   const int b = blockIdx.z;
   const int g = blockIdx.y / a.n_rowblk, rb = blockIdx.y % a.n_rowblk;
