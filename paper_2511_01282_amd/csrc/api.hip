@@ -257,7 +257,8 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
   const long long t_max = (long long)a.max_kv_len_in_batch + a.max_nodes_in_batch;
   const int per_split = a.batch * s.n_kv_heads * plan->n_rowblk;
   const int target = clampi(plan->attn_wg_target / per_split, 1, plan->nsplit_cap);
-  at.chunk = cdiv(cdiv(t_max, target), kKvTile) * kKvTile;
+  // (a split holds at least one tile per key-group wave: fewer, fuller splits for short caches)
+  at.chunk = max(cdiv(cdiv(t_max, target), kKvTile), plan->attn_shared ? plan->attn_kg : plan->wk) * kKvTile;
   at.nsplit = cdiv(t_max, at.chunk);
   at.flat = 0;
   at.batch = a.batch;
