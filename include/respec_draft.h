@@ -101,7 +101,10 @@ respec_status respec_sam_text(const respec_sam* sam, int64_t start, int32_t n, i
  * following token; the context's own trailing occurrence has none), in
  * decreasing order.  The first min(cap, total) are written to pos_out (may be
  * NULL when cap = 0) and *n_total receives the total count.  An empty result
- * means the key is not contained (Algorithm 1's SAM.Contains is false). */
+ * means the key is not contained (Algorithm 1's SAM.Contains is false).
+ * The automaton keeps the positions of recent keys (up to 8 tokens) and brings
+ * them up to date from the tokens appended since, so a query updates internal
+ * state: concurrent queries on one automaton need external synchronisation. */
 respec_status respec_sam_positions(const respec_sam* sam, const int32_t* key, int32_t k, int32_t* pos_out,
                                    int32_t cap, int32_t* n_total);
 
@@ -132,7 +135,8 @@ int64_t respec_scores_size(const respec_scores* sc);
  * position descending (the more recent occurrence first), and write the first
  * min(n_select, kept) to sel_out[RESPEC_DRAFT_MAX_SELECT]; *n_sel receives the
  * count.  pos[0..n-1] must be distinct.  Errors: RESPEC_ERR_NULL,
- * RESPEC_ERR_SHAPE (n < 0), RESPEC_ERR_PARAM (parameters out of range). */
+ * RESPEC_ERR_SHAPE (n < 0 or a negative position), RESPEC_ERR_PARAM (parameters
+ * out of range). */
 respec_status respec_select(const respec_scores* sc, const int32_t* pos, int32_t n, const respec_select_params* p,
                             int32_t* sel_out, int32_t* n_sel);
 
@@ -142,7 +146,7 @@ respec_status respec_select(const respec_scores* sc, const int32_t* pos, int32_t
  * S starting at s0.  winner = -1 means no candidate won; otherwise
  * 0 <= winner < n_sel, l_draft[winner] >= 1 and 0 <= l_acc <= l_draft[winner]
  * (RESPEC_ERR_SHAPE otherwise; l_draft may be NULL when winner = -1).
- * sel[0..n_sel-1] must be distinct. */
+ * sel[0..n_sel-1] must be distinct positions >= 0 (RESPEC_ERR_SHAPE). */
 respec_status respec_scores_update(respec_scores* sc, const int32_t* sel, int32_t n_sel, int32_t winner,
                                    int32_t l_acc, const int32_t* l_draft, const respec_select_params* p);
 

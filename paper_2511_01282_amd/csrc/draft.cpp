@@ -9,6 +9,7 @@
 
 #include <algorithm>
 #include <new>
+#include <string>
 #include <unordered_map>
 #include <utility>
 #include <vector>
@@ -76,6 +77,46 @@ class EdgeMap {
 
   std::vector<uint64_t> keys_;
   std::vector<int32_t> vals_;
+  size_t mask_ = 0, used_ = 0;
+};
+
+// Score table: open addressing over positions (>= 0), double values.
+class ScoreMap {
+ public:
+  ScoreMap() { rehash(256); }
+  double get(int32_t pos, double s0) const {
+    for (size_t i = slot(pos);; i = (i + 1) & mask_) {
+      if (keys_[i] == pos) return vals_[i];
+      if (keys_[i] == kEmpty) return s0;
+    }
+  }
+  void put(int32_t pos, double v) {
+    if (2 * (used_ + 1) > keys_.size()) rehash(keys_.size() * 2);
+    size_t i = slot(pos);
+    while (keys_[i] != kEmpty && keys_[i] != pos) i = (i + 1) & mask_;
+    if (keys_[i] == kEmpty) ++used_;
+    keys_[i] = pos;
+    vals_[i] = v;
+  }
+  size_t size() const { return used_; }
+
+ private:
+  static constexpr int32_t kEmpty = -1;
+  size_t slot(int32_t pos) const { return ((uint32_t)pos * 0x9E3779B1u) & mask_; }
+  void rehash(size_t cap) {
+    std::vector<int32_t> ok;
+    std::vector<double> ov;
+    ok.swap(keys_);
+    ov.swap(vals_);
+    keys_.assign(cap, kEmpty);
+    vals_.assign(cap, 0.0);
+    mask_ = cap - 1;
+    used_ = 0;
+    for (size_t i = 0; i < ok.size(); ++i)
+      if (ok[i] != kEmpty) put(ok[i], ov[i]);
+  }
+  std::vector<int32_t> keys_;
+  std::vector<double> vals_;
   size_t mask_ = 0, used_ = 0;
 };
 
@@ -184,6 +225,51 @@ struct respec_sam {
     return s;
   }
 
+  // Retrieval positions of a key, ascending, kept per key and brought up to
+  // date by scanning only the tokens appended since the last query (the
+  // positions found earlier stay valid: the context only grows).  Keys that
+  // repeat from step to step then cost the new tokens, not a walk of the
+  // state's subtree (thousands of states for a frequent token).
+  struct PosCache {
+    std::vector<int32_t> asc;
+    int64_t upto = 0;  // context length the list is complete for
+  };
+  static constexpr int kCacheMaxKey = 8;        // longer keys are not cached
+  static constexpr size_t kCacheMaxEntries = 1024;
+  mutable std::unordered_map<std::string, PosCache> pcache;
+  mutable std::vector<int32_t> scratch;
+
+  const std::vector<int32_t>& positions_asc(const int32_t* key, int32_t k) const {
+    const int64_t n = (int64_t)text.size();
+    if (k > kCacheMaxKey) {
+      const int32_t st = find(key, k);
+      scratch.clear();
+      if (st > 0) positions(st, scratch);
+      std::reverse(scratch.begin(), scratch.end());
+      return scratch;
+    }
+    const std::string id(reinterpret_cast<const char*>(key), sizeof(int32_t) * (size_t)k);
+    auto it = pcache.find(id);
+    if (it == pcache.end()) {
+      if (pcache.size() >= kCacheMaxEntries) pcache.clear();
+      PosCache e;
+      const int32_t st = find(key, k);
+      if (st > 0) positions(st, e.asc);
+      std::reverse(e.asc.begin(), e.asc.end());
+      e.upto = n;
+      return pcache.emplace(id, std::move(e)).first->second.asc;
+    }
+    PosCache& e = it->second;
+    // new positions p (an occurrence ending at p with a following token): upto-1 <= p <= n-2
+    for (int64_t p = std::max<int64_t>(e.upto - 1, k - 1); p <= n - 2; ++p) {
+      bool m = true;
+      for (int32_t i = 0; i < k && m; ++i) m = text[p - k + 1 + i] == key[i];
+      if (m) e.asc.push_back((int32_t)p);
+    }
+    e.upto = n;
+    return e.asc;
+  }
+
   // End positions of state s with a following token, in decreasing order.
   void positions(int32_t s, std::vector<int32_t>& out) const {
     out.clear();
@@ -200,11 +286,8 @@ struct respec_sam {
 };
 
 struct respec_scores {
-  std::unordered_map<int32_t, double> s;
-  double get(int32_t pos, double s0) const {
-    const auto it = s.find(pos);
-    return it == s.end() ? s0 : it->second;
-  }
+  ScoreMap s;
+  double get(int32_t pos, double s0) const { return pos < 0 ? s0 : s.get(pos, s0); }
 };
 
 struct respec_draft_session {
@@ -282,7 +365,7 @@ void ema_update(respec_scores& sc, const int32_t* sel, int32_t n_sel, int32_t wi
   for (int32_t i = 0; i < n_sel; ++i) {
     const double r = i == winner ? (double)l_acc / (double)l_draft[i] : 0.0;
     const double s = sc.get(sel[i], (double)p->s0);
-    sc.s[sel[i]] = (1.0 - a) * s + a * r;
+    sc.s.put(sel[i], (1.0 - a) * s + a * r);
   }
 }
 
@@ -384,12 +467,11 @@ respec_status respec_sam_positions(const respec_sam* sam, const int32_t* key, in
   for (int32_t i = 0; i < k; ++i)
     if (key[i] < 0) return RESPEC_ERR_TOKEN;
   try {
-    std::vector<int32_t> pos;
-    const int32_t s = sam->find(key, k);
-    if (s > 0) sam->positions(s, pos);
-    const int32_t m = std::min<int32_t>(cap, (int32_t)pos.size());
-    if (m > 0) memcpy(pos_out, pos.data(), sizeof(int32_t) * (size_t)m);
-    *n_total = (int32_t)pos.size();
+    const std::vector<int32_t>& asc = sam->positions_asc(key, k);  // ascending
+    const int32_t total = (int32_t)asc.size();
+    const int32_t m = std::min<int32_t>(cap, total);
+    for (int32_t j = 0; j < m; ++j) pos_out[j] = asc[total - 1 - j];  // most recent first
+    *n_total = total;
   } catch (...) {
     return RESPEC_ERR_CAPACITY;
   }
@@ -416,6 +498,8 @@ respec_status respec_select(const respec_scores* sc, const int32_t* pos, int32_t
                             int32_t* sel_out, int32_t* n_sel) {
   if (!sc || !p || !sel_out || !n_sel || (n > 0 && !pos)) return RESPEC_ERR_NULL;
   if (n < 0) return RESPEC_ERR_SHAPE;
+  for (int32_t i = 0; i < n; ++i)
+    if (pos[i] < 0) return RESPEC_ERR_SHAPE;
   if (!select_params_ok(p)) return RESPEC_ERR_PARAM;
   try {
     select_positions(*sc, pos, n, p, sel_out, n_sel);
@@ -429,6 +513,8 @@ respec_status respec_scores_update(respec_scores* sc, const int32_t* sel, int32_
                                    int32_t l_acc, const int32_t* l_draft, const respec_select_params* p) {
   if (!sc || !p || (n_sel > 0 && !sel) || (winner >= 0 && !l_draft)) return RESPEC_ERR_NULL;
   if (n_sel < 0 || n_sel > RESPEC_DRAFT_MAX_SELECT || winner < -1 || winner >= n_sel) return RESPEC_ERR_SHAPE;
+  for (int32_t i = 0; i < n_sel; ++i)
+    if (sel[i] < 0) return RESPEC_ERR_SHAPE;
   if (winner >= 0 && (l_draft[winner] < 1 || l_acc < 0 || l_acc > l_draft[winner])) return RESPEC_ERR_SHAPE;
   if (!select_params_ok(p)) return RESPEC_ERR_PARAM;
   try {
@@ -501,14 +587,13 @@ respec_status respec_draft_session_propose(respec_draft_session* s, int32_t* par
     // Step 1: the trigger over the entropies of the context's last l tokens
     const int32_t w = std::min(n, s->p.trigger.max_lookback);
     trigger_eval(s->entropy.data() + (n - w), w, &s->p.trigger, &r.trigger);
-    std::vector<int32_t> pos;
-    if (r.trigger.fire) {
-      const int32_t st = s->sam.find(s->sam.text.data() + (n - r.trigger.key_len), r.trigger.key_len);
-      if (st > 0) s->sam.positions(st, pos);
-    }
+    static const std::vector<int32_t> kNone;
+    const std::vector<int32_t>& pos =
+        r.trigger.fire ? s->sam.positions_asc(s->sam.text.data() + (n - r.trigger.key_len), r.trigger.key_len)
+                       : kNone;
     r.n_positions = (int32_t)pos.size();
     if (r.trigger.fire && !pos.empty()) {
-      // Step 2: quality filtering, top-n selection, BuildDraftTree
+      // Step 2: quality filtering, top-n selection (order-independent), BuildDraftTree
       select_positions(s->scores, pos.data(), (int32_t)pos.size(), &s->p.select, r.sel_pos, &r.n_selected);
       if (r.n_selected > 0) {
         build_tree(s->sam, r.sel_pos, r.n_selected, &s->p.tree, parent, token, src, &r.n_nodes, r.cand_end,

@@ -130,6 +130,15 @@ def test_selection_and_ema_parity():
                 assert sc_lib.get(p, s0) == v
 
 
+def test_negative_positions_are_rejected():
+    sc = draft.Scores()
+    with pytest.raises(binding.VerifyError):
+        sc.select([3, -1])
+    with pytest.raises(binding.VerifyError):
+        sc.update([-2], -1, 0, None)
+    assert len(sc) == 0
+
+
 def test_ema_update_errors():
     sc = draft.Scores()
     with pytest.raises(binding.VerifyError):
