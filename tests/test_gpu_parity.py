@@ -142,6 +142,7 @@ def test_edge_case_parity(rt, name):
 # row 3.5x row 7, so that on many rows the top-k is token 5 followed by equal
 # logits (more of them reach the candidate threshold than the sorted path takes).
 VOCAB_TIERS = [
+    (3001, 8, "plain"),        # a vocabulary that is not a multiple of 4 (unaligned logit rows)
     (3000, 16, "clustered"),
     (3000, 8, "tied"),
     (30000, 8, "clustered"),

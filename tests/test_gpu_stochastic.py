@@ -40,10 +40,19 @@ CASES = {
     "c4-T1": (4, 1.0, True),
     "star30-T1.5": ("star", 1.5, True),
     "ragged-T0.9": ("ragged", 0.9, True),
+    "odd-vocab-T1.1": ("odd", 1.1, True),
+    "drafter-equals-target-T0.3": ("exact", 0.3, True),
 }
 
 
 def _custom(kind):
+    if kind in ("odd", "exact"):
+        v = 3001 if kind == "odd" else 3000
+        shp = synth.Shape("edge", "bf16", 4 * 64, 4, 1, 64, v, 2, 8, 8, 8)
+        parents = [[-1, 0, 1, 1, 3, 0, 5, 5], [-1, 0, 0, 2]]
+        w = synth.custom(shp, parents, [70, 40], seed=211, poison_tail=True,
+                         src=[[0] + [j % 2 for j in range(1, len(p))] for p in parents])
+        return workload.finish(w)
     if kind == "star":
         shp = _edge_shape("bf16", 4, 2, 128)
         parents, kv = [[-1] + [0] * 30], [130]
@@ -65,7 +74,8 @@ def test_stochastic_parity(rt, name):
     spec, T, with_q = CASES[name]
     print(f"[stochastic {name}] building case", flush=True)
     case = workload.build(spec) if isinstance(spec, int) else _custom(spec)
-    q, u = workload.stochastic_inputs(case, T, with_q=with_q)
+    # "exact": the drafter's distributions are the target's own (every model draft passes)
+    q, u = workload.stochastic_inputs(case, T, with_q=with_q, q_noise=0.0 if spec == "exact" else 0.5)
     exp = workload.stochastic_expected(case, q, u, T)
     case.expected = dict(case.expected, **exp)
     case.w.params = synth.AcceptParams(case.w.params.topk, case.w.params.tau, case.w.params.min_lookahead,
