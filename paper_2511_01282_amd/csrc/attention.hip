@@ -640,8 +640,17 @@ __device__ __forceinline__ void attn_segment(const AttnArgs& a, unsigned char* s
     // pass.  The last tiles (straight-line code) refill only while tiles
     // remain: no load is left in flight for the workgroup's merge barrier to
     // wait for.
+    // A wave with at most two tiles (short splits) requests the second one at
+    // once: it then waits for one memory latency instead of two in a row.
+    // (Past the last tile the request repeats the last row: cached, unused.)
+    if (n_tiles <= 2) {
+      load_k_bf16<D>(kb, kbase, tile_row(1), kv_hi, lane);
+      load_v_bf16<D>(vb, vbase, tile_row(1), kv_hi, lane);
+      if (n_tiles > 0) tile_step(ka, va, 0, false, false);
+      if (n_tiles > 1) tile_step(kb, vb, 1, false, false);
+    } else {
     int i = 1;
-    if (n_tiles > 0) tile_step(ka, va, 0, 2 < n_tiles, true);
+    tile_step(ka, va, 0, 2 < n_tiles, true);
     for (; i + 4 <= n_tiles; i += 2) {
       tile_step(kb, vb, i, true, false);
       tile_step(ka, va, i + 1, true, false);
@@ -649,6 +658,7 @@ __device__ __forceinline__ void attn_segment(const AttnArgs& a, unsigned char* s
     if (i < n_tiles) tile_step(kb, vb, i, i + 2 < n_tiles, false);
     if (i + 1 < n_tiles) tile_step(ka, va, i + 1, i + 3 < n_tiles, false);
     if (i + 2 < n_tiles) tile_step(kb, vb, i + 2, false, false);
+    }
   } else {
     // float32: registers hold one tile; V is transposed through LDS by the VALU
     if (kv_hi > L)
