@@ -1086,31 +1086,13 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   constexpr int kBatch = 8;         // splits requested per batch
   const int bgr = blockIdx.y;
   const int rb = bgr % a.n_rowblk, g = (bgr / a.n_rowblk) % a.n_kv_heads, b = bgr / (a.n_rowblk * a.n_kv_heads);
-  const int rl = blockIdx.x * kRows + (int)threadIdx.x / D4;  // row within the row block
-  const int d = ((int)threadIdx.x % D4) * 4;
-  const size_t sbase = (size_t)bgr * a.nsplit * a.rows_per_wg + min(rl, a.rows_per_wg - 1);
-  const size_t sstride = (size_t)a.rows_per_wg;
-  // The first batch of partials is requested before the node offsets arrive: the slots'
-  // addresses do not depend on them (slots past the sequence's count, and the rows of threads
-  // past the row block, are read and then ignored).
-  float mv[kBatch], lv[kBatch];
-  f32x4 ov[kBatch];
-  auto request = [&](int sp0) {
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const int sp = sp0 + u;
-      const size_t pr = sbase + (size_t)(sp < a.nsplit ? sp : 0) * sstride;
-      mv[u] = a.part_m[pr];
-      lv[u] = a.part_l[pr];
-      ov[u] = *reinterpret_cast<const f32x4*>(a.part_o + pr * D + d);
-    }
-  };
-  request(0);
   const int node0 = a.node_off[b], node1 = a.node_off[b + 1];
   int n_nodes = node1 - node0;
   if (node0 < 0 || node1 > a.total_nodes || n_nodes < 1 || n_nodes > a.max_nodes) n_nodes = 0;
   const int R = n_nodes * a.group;
   const int row_wg = rb * a.rows_per_wg;
+  const int rl = blockIdx.x * kRows + (int)threadIdx.x / D4;  // row within the row block
+  const int d = ((int)threadIdx.x % D4) * 4;
   // partials of this sequence: every split, or (flat partition) the pieces its tiles span
   int nsp = a.nsplit;
   if (a.flat) {
@@ -1119,6 +1101,8 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     nsp = nt > 0 ? flat_piece(pre + nt - 1, a.flat, ft.total) - flat_piece(pre, a.flat, ft.total) + 1 : 0;
   }
   if (rl >= a.rows_per_wg || row_wg + rl >= R) return;
+  const size_t sbase = (size_t)bgr * a.nsplit * a.rows_per_wg + rl;
+  const size_t sstride = (size_t)a.rows_per_wg;
 
   const int rr = row_wg + rl;
   const int node = rr / a.group;
@@ -1131,13 +1115,16 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   float M = kNegInf, Ls = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   for (int sp0 = 0; sp0 < nsp; sp0 += kBatch) {
-    if (sp0 > 0) request(sp0);
+    float mv[kBatch], lv[kBatch];
+    f32x4 ov[kBatch];
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
-      if (sp0 + u < nsp) continue;
-      mv[u] = kNegInf;
-      lv[u] = 0.f;
-      ov[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int sp = sp0 + u;
+      const bool ok = sp < nsp;
+      const size_t pr = sbase + (size_t)(ok ? sp : 0) * sstride;
+      mv[u] = ok ? a.part_m[pr] : kNegInf;
+      lv[u] = ok ? a.part_l[pr] : 0.f;
+      ov[u] = ok ? *reinterpret_cast<const f32x4*>(a.part_o + pr * D + d) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
     // running merge: rescale what is accumulated to the new maximum
     float Mb = M;
