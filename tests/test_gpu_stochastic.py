@@ -27,10 +27,6 @@ def rt():
     return runner
 
 
-def _star(w):
-    return w
-
-
 CASES = {
     # name: (config or custom tree spec, temperature, drafter distributions given)
     "c0-T1": (0, 1.0, True),
