@@ -53,7 +53,8 @@ typedef enum {
   RESPEC_ERR_CAPACITY = 6,  /* batch / nodes / KV length above the plan's capacity          */
   RESPEC_ERR_HIP = 7,       /* a HIP call or kernel launch failed                            */
   RESPEC_ERR_WORKSPACE = 8, /* workspace missing or not 256-byte aligned                    */
-  RESPEC_ERR_TOKEN = 9      /* seq_status only: a draft token or source tag is out of range */
+  RESPEC_ERR_TOKEN = 9,     /* seq_status only: a draft token or source tag is out of range */
+  RESPEC_ERR_SCRATCH = 10   /* respec_verify_step_noalloc: the plan does not fit the static scratch */
 } respec_status;
 
 typedef enum { RESPEC_F32 = 0, RESPEC_BF16 = 1 } respec_dtype;
@@ -79,6 +80,14 @@ enum { RESPEC_STOP_ALL = 0, RESPEC_STOP_ATTN = 1, RESPEC_STOP_LOGITS = 2 };
 
 /* Limits of this implementation. */
 enum { RESPEC_MAX_NODES = 128, RESPEC_MAX_DEPTH = 64, RESPEC_MAX_TOPK_OUT = 16 };
+
+/* Static scratch of respec_verify_step_noalloc: 64 MiB of device memory per GPU
+ * (the front 64 KiB hold one completion counter per sequence, the rest the
+ * plan's workspace), so plans with respec_verify_workspace_bytes() up to
+ * RESPEC_NOALLOC_SCRATCH_BYTES - 4 * RESPEC_NOALLOC_MAX_BATCH and max_batch up
+ * to RESPEC_NOALLOC_MAX_BATCH. */
+#define RESPEC_NOALLOC_SCRATCH_BYTES (64u << 20)
+#define RESPEC_NOALLOC_MAX_BATCH 16384
 
 /* Shapes and capacities, fixed when the plan is created. */
 typedef struct {
@@ -210,6 +219,25 @@ respec_status respec_verify_check_tree(const int32_t* parent_host, int32_t n, in
  * respec_verify_workspace_init. */
 respec_status respec_verify_step(const respec_verify_plan* plan, const respec_verify_args* args,
                                  void* workspace, void* stream);
+
+/* Allocation-free form of respec_verify_step, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, launches and results as
+ * respec_verify_step, except that the workspace is not passed: the step uses a
+ * static device array inside the library (RESPEC_NOALLOC_SCRATCH_BYTES, one per
+ * GPU, held by every GPU the library runs on until the process ends).  The
+ * first call on a device, with that device current, looks the array up and
+ * clears its completion counters with a kernel enqueued on stream; no call
+ * allocates or frees memory.  Returns RESPEC_ERR_SCRATCH, launching nothing,
+ * when respec_verify_workspace_bytes(plan) exceeds
+ * RESPEC_NOALLOC_SCRATCH_BYTES - 4 * RESPEC_NOALLOC_MAX_BATCH or the plan's
+ * max_batch exceeds RESPEC_NOALLOC_MAX_BATCH; RESPEC_ERR_HIP when the array
+ * cannot be looked up.  Every call on a GPU shares that GPU's array, which
+ * keeps the last call's intermediates: calls that overlap on one GPU (other
+ * streams or threads, without ordering between them) race, and the caller
+ * must serialise them. */
+respec_status respec_verify_step_noalloc(const respec_verify_plan* plan, const respec_verify_args* args,
+                                         void* stream);
 
 /* Static description of a status code. */
 const char* respec_status_string(respec_status status);

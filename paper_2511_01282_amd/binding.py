@@ -15,7 +15,9 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "librespec_verify.so")
 
-OK, ERR_NULL, ERR_SHAPE, ERR_DTYPE, ERR_PARAM, ERR_TREE, ERR_CAPACITY, ERR_HIP, ERR_WORKSPACE, ERR_TOKEN = range(10)
+(OK, ERR_NULL, ERR_SHAPE, ERR_DTYPE, ERR_PARAM, ERR_TREE, ERR_CAPACITY, ERR_HIP, ERR_WORKSPACE, ERR_TOKEN,
+ ERR_SCRATCH) = range(11)
+NOALLOC_SCRATCH_BYTES, NOALLOC_MAX_BATCH = 64 << 20, 16384
 F32, BF16 = 0, 1
 SRC_MODEL, SRC_RETRIEVED = 0, 1
 FLAG_GREEDY, FLAG_TOPK, FLAG_TAU, FLAG_RELAXED, FLAG_ON_PATH, FLAG_STOCH_ACCEPT = 1, 2, 4, 8, 16, 32
@@ -25,7 +27,7 @@ MAX_NODES, MAX_DEPTH, MAX_TOPK_OUT = 128, 64, 16
 EXPORTS = (
     "respec_verify_create", "respec_verify_destroy", "respec_verify_workspace_bytes",
     "respec_verify_workspace_init", "respec_verify_check_tree", "respec_verify_step",
-    "respec_status_string",
+    "respec_verify_step_noalloc", "respec_status_string",
 )
 
 
@@ -88,6 +90,8 @@ def lib() -> ctypes.CDLL:
         L.respec_verify_check_tree.restype = ctypes.c_int
         L.respec_verify_step.argtypes = [ctypes.c_void_p, ctypes.POINTER(Args), ctypes.c_void_p, ctypes.c_void_p]
         L.respec_verify_step.restype = ctypes.c_int
+        L.respec_verify_step_noalloc.argtypes = [ctypes.c_void_p, ctypes.POINTER(Args), ctypes.c_void_p]
+        L.respec_verify_step_noalloc.restype = ctypes.c_int
         L.respec_status_string.argtypes = [ctypes.c_int]
         L.respec_status_string.restype = ctypes.c_char_p
         _LIB = L
@@ -171,8 +175,12 @@ class Plan:
 
     def step(self, inputs: dict, outputs: dict, *, batch, total_nodes, max_nodes_in_batch,
              max_kv_len_in_batch, kv_capacity, topk=8, tau=3.0, min_lookahead=2, max_relaxed=2,
-             stochastic=0, temperature=1.0, stop_after=STOP_ALL, stream=None, stage_events=None) -> None:
-        """Enqueue one verification step (asynchronous, on ``stream``)."""
+             stochastic=0, temperature=1.0, stop_after=STOP_ALL, stream=None, stage_events=None,
+             noalloc=False) -> None:
+        """Enqueue one verification step (asynchronous, on ``stream``).
+
+        ``noalloc``: call respec_verify_step_noalloc (the library's static scratch
+        instead of this plan's workspace)."""
         a = Args()
         a.batch, a.total_nodes = batch, total_nodes
         a.max_nodes_in_batch, a.max_kv_len_in_batch = max_nodes_in_batch, max_kv_len_in_batch
@@ -186,8 +194,12 @@ class Plan:
         if stage_events is not None:
             ev_arr = (ctypes.c_void_p * 4)(*[e.cuda_event for e in stage_events])
             a.stage_events = ctypes.cast(ev_arr, ctypes.c_void_p)
-        _check(lib().respec_verify_step(self._h, ctypes.byref(a), self.workspace_ptr, self._stream(stream)),
-               "respec_verify_step")
+        if noalloc:
+            _check(lib().respec_verify_step_noalloc(self._h, ctypes.byref(a), self._stream(stream)),
+                   "respec_verify_step_noalloc")
+        else:
+            _check(lib().respec_verify_step(self._h, ctypes.byref(a), self.workspace_ptr, self._stream(stream)),
+                   "respec_verify_step")
 
 
 def alloc_outputs(*, total_nodes, batch, hidden, vocab, topk_out, max_depth, device="cuda",

@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <mutex>
 #include <new>
 
 #include "../../include/respec_verify.h"
@@ -60,6 +61,7 @@ const char* respec_status_string(respec_status st) {
     case RESPEC_ERR_HIP: return "HIP call or kernel launch failed";
     case RESPEC_ERR_WORKSPACE: return "workspace missing or not 256-byte aligned";
     case RESPEC_ERR_TOKEN: return "draft token or source tag out of range";
+    case RESPEC_ERR_SCRATCH: return "plan needs more workspace or sequences than the static scratch of the allocation-free step holds";
   }
   return "unknown status";
 }
@@ -180,12 +182,16 @@ respec_status respec_verify_workspace_init(const respec_verify_plan* plan, void*
   return launch_zero_i32(cnt, n, static_cast<hipStream_t>(stream)) == hipSuccess ? RESPEC_OK : RESPEC_ERR_HIP;
 }
 
-respec_status respec_verify_step(const respec_verify_plan* plan, const respec_verify_args* args, void* workspace,
-                                 void* stream) {
-  if (!plan || !args) return RESPEC_ERR_NULL;
+}  // extern "C"
+
+namespace {
+
+// One step on workspace `ws` (the plan's layout) with the sequences' completion
+// counters at `cnt` (zero between steps).
+respec_status step_impl(const respec_verify_plan* plan, const respec_verify_args* args, char* ws, int32_t* cnt,
+                        void* stream) {
   const respec_verify_shape& s = plan->s;
   const respec_verify_args& a = *args;
-  if (!workspace || !aligned(workspace, 256)) return RESPEC_ERR_WORKSPACE;
   if (a.stop_after < RESPEC_STOP_ALL || a.stop_after > RESPEC_STOP_LOGITS) return RESPEC_ERR_PARAM;
   if (a.batch < 0) return RESPEC_ERR_SHAPE;
   if (a.batch > s.max_batch) return RESPEC_ERR_CAPACITY;
@@ -225,8 +231,6 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
       (need_logits && (!aligned(a.lm_head, 16) || !aligned(a.logits, 16))) || (a.attn_out && !aligned(a.attn_out, 16)))
     return RESPEC_ERR_SHAPE;
 
-  char* ws = static_cast<char*>(workspace);
-  int32_t* cnt = reinterpret_cast<int32_t*>(ws + plan->off_cnt);
 
   if (!plan->lds_ready.load(std::memory_order_acquire)) {
     const hipError_t e = plan->attn_shared ? set_tree_attn_shared_lds_limit(s.head_dim, plan->attn_stages, plan->attn_kg, plan->attn_lds)
@@ -392,6 +396,63 @@ respec_status respec_verify_step(const respec_verify_plan* plan, const respec_ve
     return RESPEC_ERR_HIP;
   }
   return RESPEC_OK;
+}
+
+// ---- static workspace of the allocation-free entry point ----
+// The array's name is a host-side stand-in: host code uses the device address
+// that hipGetSymbolAddress returns for the current device, never `scratch`.
+// The front kScratchCounterBytes hold the completion counters at a fixed place,
+// so that plans with different workspace layouts sharing the array never read
+// another plan's leftovers as counters; the plan's workspace follows them.
+constexpr size_t kScratchBytes = (size_t)RESPEC_NOALLOC_SCRATCH_BYTES;
+constexpr size_t kScratchCounterBytes = (size_t)RESPEC_NOALLOC_MAX_BATCH * 4;
+static_assert(kScratchCounterBytes % 256 == 0, "the workspace after the counters stays 256-byte aligned");
+constexpr int kMaxDevices = 64;
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+struct ScratchSlot {
+  std::once_flag once;
+  char* ptr = nullptr;  // device address of `scratch` on this device (null: set-up failed)
+};
+ScratchSlot g_scratch[kMaxDevices];
+
+// Device address of this device's array; on the first call on a device (with
+// that device current) it is looked up and the counters are cleared by a fill
+// kernel on `stream` (no memset node, so a captured first call stays correct).
+char* scratch_for_current_device(hipStream_t stream) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  ScratchSlot& sl = g_scratch[dev];
+  std::call_once(sl.once, [&] {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return;
+    if (launch_zero_i32(static_cast<int32_t*>(p), RESPEC_NOALLOC_MAX_BATCH, stream) != hipSuccess) return;
+    sl.ptr = static_cast<char*>(p);
+  });
+  return sl.ptr;
+}
+
+}  // namespace
+
+extern "C" {
+
+respec_status respec_verify_step(const respec_verify_plan* plan, const respec_verify_args* args, void* workspace,
+                                 void* stream) {
+  if (!plan || !args) return RESPEC_ERR_NULL;
+  if (!workspace || !aligned(workspace, 256)) return RESPEC_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  return step_impl(plan, args, ws, reinterpret_cast<int32_t*>(ws + plan->off_cnt), stream);
+}
+
+respec_status respec_verify_step_noalloc(const respec_verify_plan* plan, const respec_verify_args* args,
+                                         void* stream) {
+  if (!plan || !args) return RESPEC_ERR_NULL;
+  if (plan->total > kScratchBytes - kScratchCounterBytes || plan->s.max_batch > RESPEC_NOALLOC_MAX_BATCH)
+    return RESPEC_ERR_SCRATCH;
+  char* base = scratch_for_current_device(static_cast<hipStream_t>(stream));
+  if (!base) return RESPEC_ERR_HIP;
+  return step_impl(plan, args, base + kScratchCounterBytes, reinterpret_cast<int32_t*>(base), stream);
 }
 
 }  // extern "C"

@@ -38,7 +38,7 @@ def test_library_exports_every_declared_function(b):
 
 
 def test_status_strings(b):
-    for code in range(10):
+    for code in range(11):
         assert b.status_string(code)
     assert b.status_string(0) == "ok"
 
