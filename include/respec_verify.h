@@ -75,8 +75,13 @@ enum {
                                    the speculative-sampling test (see respec_accept_params)   */
 };
 
-/* stop_after (debugging and per-stage timing) */
-enum { RESPEC_STOP_ALL = 0, RESPEC_STOP_ATTN = 1, RESPEC_STOP_LOGITS = 2 };
+/* stop_after (debugging and per-stage timing).  ATTN: attention and residual
+ * only (attn_out, x_out); LOGITS: also the LM head (logits); STATS: also the
+ * per-row statistics and per-node predicates (max_logit, lse, entropy, argmax,
+ * topk_id, topk_logprob, tok_logprob, tok_rank, flags without ON_PATH), but no
+ * path reduction (leaf_acc_len, path, acc_len, bonus, winner_leaf, seq_status
+ * and sample are not written and may be NULL); ALL: the whole step. */
+enum { RESPEC_STOP_ALL = 0, RESPEC_STOP_ATTN = 1, RESPEC_STOP_LOGITS = 2, RESPEC_STOP_STATS = 3 };
 
 /* Limits of this implementation. */
 enum { RESPEC_MAX_NODES = 128, RESPEC_MAX_DEPTH = 64, RESPEC_MAX_TOPK_OUT = 16 };
@@ -167,6 +172,8 @@ typedef struct {
 
   /* outputs (device) */
   float* attn_out;          /* [M][Hd] float32 attention output O, or NULL                 */
+  void* x_out;              /* [M][Hd] dtype residual x = round(h + O) that feeds the LM
+                               head (round to nearest even for bf16), or NULL              */
   float* logits;            /* [M][V] float32 logits z (required unless STOP_ATTN)         */
   float* max_logit;         /* [M] max_v z                                                  */
   float* lse;               /* [M] log sum_v exp z                                          */
@@ -175,6 +182,11 @@ typedef struct {
   int32_t* topk_id;         /* [M][topk_out] ids by (z desc, id asc)                        */
   float* topk_logprob;      /* [M][topk_out] log p of those ids                             */
   float* tok_logprob;       /* [M] log p_parent(t_j); 0 for roots                           */
+  int32_t* tok_rank;        /* [M] rank of t_j in its parent's logits z_i, or NULL (not
+                               computed; no decision depends on it, the TOPK flag holds
+                               rank < k):  #{u : z_i[u] > z_i[t_j]} + #{u < t_j : z_i[u] ==
+                               z_i[t_j]} on the float32 logits (0 = the argmax); -1 for
+                               roots and for nodes without a valid parent or token        */
   uint8_t* flags;           /* [M] RESPEC_FLAG_* bits                                       */
   int32_t* leaf_acc_len;    /* [M] accepted length of each leaf's chain, -1 for inner nodes */
   int32_t* path;            /* [B][max_depth+1] sequence-local node ids of the accepted path,

@@ -21,7 +21,7 @@ NOALLOC_SCRATCH_BYTES, NOALLOC_MAX_BATCH = 64 << 20, 16384
 F32, BF16 = 0, 1
 SRC_MODEL, SRC_RETRIEVED = 0, 1
 FLAG_GREEDY, FLAG_TOPK, FLAG_TAU, FLAG_RELAXED, FLAG_ON_PATH, FLAG_STOCH_ACCEPT = 1, 2, 4, 8, 16, 32
-STOP_ALL, STOP_ATTN, STOP_LOGITS = 0, 1, 2
+STOP_ALL, STOP_ATTN, STOP_LOGITS, STOP_STATS = 0, 1, 2, 3
 MAX_NODES, MAX_DEPTH, MAX_TOPK_OUT = 128, 64, 16
 
 EXPORTS = (
@@ -54,8 +54,9 @@ class Args(ctypes.Structure):
         ("accept", AcceptParams),
         ("node_off", _P), ("kv_len", _P), ("hidden", _P), ("k_cache", _P), ("v_cache", _P),
         ("lm_head", _P), ("parent", _P), ("token", _P), ("src", _P), ("draft_prob", _P), ("uniform", _P),
-        ("attn_out", _P), ("logits", _P), ("max_logit", _P), ("lse", _P), ("entropy", _P),
-        ("argmax", _P), ("topk_id", _P), ("topk_logprob", _P), ("tok_logprob", _P), ("flags", _P),
+        ("attn_out", _P), ("x_out", _P), ("logits", _P), ("max_logit", _P), ("lse", _P), ("entropy", _P),
+        ("argmax", _P), ("topk_id", _P), ("topk_logprob", _P), ("tok_logprob", _P), ("tok_rank", _P),
+        ("flags", _P),
         ("leaf_acc_len", _P), ("path", _P), ("acc_len", _P), ("bonus", _P), ("winner_leaf", _P),
         ("seq_status", _P), ("sample", _P), ("stage_events", _P),
     ]
@@ -63,9 +64,9 @@ class Args(ctypes.Structure):
 
 INPUT_FIELDS = ("node_off", "kv_len", "hidden", "k_cache", "v_cache", "lm_head", "parent", "token", "src",
                 "draft_prob", "uniform")
-OUTPUT_FIELDS = ("attn_out", "logits", "max_logit", "lse", "entropy", "argmax", "topk_id", "topk_logprob",
-                 "tok_logprob", "flags", "leaf_acc_len", "path", "acc_len", "bonus", "winner_leaf",
-                 "seq_status", "sample")
+OUTPUT_FIELDS = ("attn_out", "x_out", "logits", "max_logit", "lse", "entropy", "argmax", "topk_id",
+                 "topk_logprob", "tok_logprob", "tok_rank", "flags", "leaf_acc_len", "path", "acc_len", "bonus",
+                 "winner_leaf", "seq_status", "sample")
 
 _LIB = None
 
@@ -203,12 +204,16 @@ class Plan:
 
 
 def alloc_outputs(*, total_nodes, batch, hidden, vocab, topk_out, max_depth, device="cuda",
-                  attn_out=True) -> dict:
+                  attn_out=True, x_dtype=None, tok_rank=False) -> dict:
+    """Output tensors of one step.  ``x_dtype`` (torch.bfloat16 / torch.float32): also
+    return the residual x; ``tok_rank``: also the exact ranks of the draft tokens."""
     M, B = total_nodes, batch
     f32 = dict(dtype=torch.float32, device=device)
     i32 = dict(dtype=torch.int32, device=device)
     return {
         "attn_out": torch.empty(M, hidden, **f32) if attn_out else None,
+        "x_out": torch.empty(M, hidden, dtype=x_dtype, device=device) if x_dtype is not None else None,
+        "tok_rank": torch.empty(M, **i32) if tok_rank else None,
         "logits": torch.empty(M, vocab, **f32),
         "max_logit": torch.empty(M, **f32), "lse": torch.empty(M, **f32), "entropy": torch.empty(M, **f32),
         "argmax": torch.empty(M, **i32),

@@ -29,7 +29,7 @@ struct respec_verify_plan {
   // vocabulary statistics: tiles of the LM head and the top-K width (8 or 16)
   int ko, n_vtiles;
   // workspace layout (bytes)
-  size_t off_po, off_pm, off_pl, off_x, off_part, off_flag, off_cnt, off_stoch;
+  size_t off_po, off_pm, off_pl, off_x, off_part, off_flag, off_cnt, off_stoch, off_rank;
   size_t n_cnt_seq, total;
   // the attention kernel's LDS limit is raised on the first step (plan creation stays GPU-free)
   mutable std::atomic<bool> lds_ready{false};
@@ -164,6 +164,7 @@ respec_status respec_verify_create(const respec_verify_shape* shape, respec_veri
   p->n_cnt_seq = s.max_batch;
   p->off_cnt = off; off = align256(off + p->n_cnt_seq * 4);
   p->off_stoch = off; off = align256(off + 2 * mcap * 4);  // stochastic walk: next child, draw
+  p->off_rank = off; off = align256(off + mcap * 4);       // rank requests: parent row per node
   p->total = off;
 
   *out = p;
@@ -192,12 +193,14 @@ respec_status step_impl(const respec_verify_plan* plan, const respec_verify_args
                         void* stream) {
   const respec_verify_shape& s = plan->s;
   const respec_verify_args& a = *args;
-  if (a.stop_after < RESPEC_STOP_ALL || a.stop_after > RESPEC_STOP_LOGITS) return RESPEC_ERR_PARAM;
+  if (a.stop_after < RESPEC_STOP_ALL || a.stop_after > RESPEC_STOP_STATS) return RESPEC_ERR_PARAM;
   if (a.batch < 0) return RESPEC_ERR_SHAPE;
   if (a.batch > s.max_batch) return RESPEC_ERR_CAPACITY;
   const bool full = a.stop_after == RESPEC_STOP_ALL;
+  const bool stats_only = a.stop_after == RESPEC_STOP_STATS;
+  const bool vocab_pass = full || stats_only;  // statistics and predicates run
   const bool need_logits = a.stop_after != RESPEC_STOP_ATTN;
-  if (full) {
+  if (vocab_pass) {
     const respec_accept_params& q = a.accept;
     if (q.topk < 1 || q.topk > s.topk_out || !(q.tau >= 0.f) || isinf(q.tau) || q.min_lookahead < 0 ||
         q.max_relaxed < 0 || (q.stochastic != 0 && q.stochastic != 1))
@@ -221,15 +224,17 @@ respec_status step_impl(const respec_verify_plan* plan, const respec_verify_args
   if ((long long)a.kv_capacity < (long long)a.max_kv_len_in_batch + a.max_nodes_in_batch) return RESPEC_ERR_SHAPE;
   if (!a.node_off || !a.kv_len || !a.hidden || !a.k_cache || !a.v_cache || !a.parent) return RESPEC_ERR_NULL;
   if (need_logits && (!a.lm_head || !a.logits)) return RESPEC_ERR_NULL;
-  if (full && (!a.token || !a.src || !a.max_logit || !a.lse || !a.entropy || !a.argmax || !a.topk_id ||
-               !a.topk_logprob || !a.tok_logprob || !a.flags || !a.leaf_acc_len || !a.path || !a.acc_len ||
-               !a.bonus || !a.winner_leaf || !a.seq_status))
+  if (vocab_pass && (!a.token || !a.src || !a.max_logit || !a.lse || !a.entropy || !a.argmax || !a.topk_id ||
+                     !a.topk_logprob || !a.tok_logprob || !a.flags))
+    return RESPEC_ERR_NULL;
+  if (full && (!a.leaf_acc_len || !a.path || !a.acc_len || !a.bonus || !a.winner_leaf || !a.seq_status))
     return RESPEC_ERR_NULL;
   if (stochastic && !a.uniform) return RESPEC_ERR_NULL;
   if (stochastic && a.draft_prob && !aligned(a.draft_prob, 16)) return RESPEC_ERR_SHAPE;
   if (!aligned(a.hidden, 16) || !aligned(a.k_cache, 16) || !aligned(a.v_cache, 16) ||
       (need_logits && (!aligned(a.lm_head, 16) || !aligned(a.logits, 16))) || (a.attn_out && !aligned(a.attn_out, 16)))
     return RESPEC_ERR_SHAPE;
+  const bool rank = vocab_pass && a.tok_rank != nullptr;
 
 
   if (!plan->lds_ready.load(std::memory_order_acquire)) {
@@ -252,6 +257,7 @@ respec_status step_impl(const respec_verify_plan* plan, const respec_verify_args
   at.part_l = reinterpret_cast<float*>(ws + plan->off_pl);
   at.x_out = ws + plan->off_x;
   at.attn_out = a.attn_out;
+  at.x_copy = a.x_out;
   at.total_nodes = a.total_nodes;
   at.hidden_size = s.hidden;
   at.n_kv_heads = s.n_kv_heads;
@@ -311,7 +317,7 @@ respec_status step_impl(const respec_verify_plan* plan, const respec_verify_args
     if (M > 64 && s.dtype == RESPEC_BF16) mb = M <= 128 ? 8 : 16;
     const bool wide = s.dtype == RESPEC_BF16 && M <= 64 && plan->n_vtiles > 2 * kCUs;
     lm.n_mtiles = wide ? 1 : cdiv(M, 16 * mb);
-    lm.partials = full ? reinterpret_cast<float*>(ws + plan->off_part) : nullptr;
+    lm.partials = vocab_pass ? reinterpret_cast<float*>(ws + plan->off_part) : nullptr;
     lm.n_vtiles = plan->n_vtiles;
     if (launch_lmhead(s.dtype, mb, wide, lm, st, ev ? ev[2] : nullptr) != hipSuccess) return RESPEC_ERR_HIP;
   } else if (ev && hipEventRecord(ev[2], st) != hipSuccess) {
@@ -319,7 +325,7 @@ respec_status step_impl(const respec_verify_plan* plan, const respec_verify_args
   }
 
   // ---- row statistics, predicates, path ----
-  if (full) {
+  if (vocab_pass) {
     VocabArgs v;
     v.logits = a.logits;
     v.partials = reinterpret_cast<const float*>(ws + plan->off_part);
@@ -357,7 +363,11 @@ respec_status step_impl(const respec_verify_plan* plan, const respec_verify_args
     v.min_lookahead = a.accept.min_lookahead;
     v.max_relaxed = a.accept.max_relaxed;
     v.tau = a.accept.tau;
-    if (launch_finalize(plan->ko, a.total_nodes + a.batch, v, st, (ev && !stochastic) ? ev[3] : nullptr) !=
+    v.stats_only = stats_only;
+    v.rank_req = rank ? reinterpret_cast<int32_t*>(ws + plan->off_rank) : nullptr;
+    v.tok_rank = rank ? a.tok_rank : nullptr;
+    // (the stage's last kernel takes the stop event: the rank pass, else the sampling walk, else this one)
+    if (launch_finalize(plan->ko, a.total_nodes + a.batch, v, st, (ev && !stochastic && !rank) ? ev[3] : nullptr) !=
         hipSuccess)
       return RESPEC_ERR_HIP;
     if (stochastic) {
@@ -390,7 +400,17 @@ respec_status step_impl(const respec_verify_plan* plan, const respec_verify_args
       sa.max_depth = s.max_depth;
       sa.inv_temp = 1.f / a.accept.temperature;
       sa.unit_temp = a.accept.temperature == 1.f;
-      if (launch_stochastic(sa, st, ev ? ev[3] : nullptr) != hipSuccess) return RESPEC_ERR_HIP;
+      if (launch_stochastic(sa, st, (ev && !rank) ? ev[3] : nullptr) != hipSuccess) return RESPEC_ERR_HIP;
+    }
+    if (rank) {
+      RankArgs ra;
+      ra.logits = a.logits;
+      ra.token = a.token;
+      ra.rank_req = v.rank_req;
+      ra.tok_rank = a.tok_rank;
+      ra.total_nodes = a.total_nodes;
+      ra.vocab = s.vocab;
+      if (launch_rank(ra, st, ev ? ev[3] : nullptr) != hipSuccess) return RESPEC_ERR_HIP;
     }
   } else if (ev && hipEventRecord(ev[3], st) != hipSuccess) {
     return RESPEC_ERR_HIP;

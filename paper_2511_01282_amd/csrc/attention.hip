@@ -1145,7 +1145,11 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   acc *= inv;
   if (a.attn_out) *reinterpret_cast<f32x4*>(a.attn_out + gi) = acc;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) Elem<T>::store(a.x_out, gi + i, hv[i] + acc[i]);
+  for (int i = 0; i < 4; ++i) Elem<T>::store_sum(a.x_out, gi + i, hv[i], acc[i]);
+  if (a.x_copy) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) Elem<T>::store_sum(a.x_copy, gi + i, hv[i], acc[i]);
+  }
 }
 
 template <typename T, int D>

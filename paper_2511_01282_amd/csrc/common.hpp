@@ -37,6 +37,21 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// bf16 of the exact sum a + b, round to nearest even.  The float32 sum s and
+// its rounding error e are exact (TwoSum); rounding s again to bf16 can only
+// differ from rounding a + b once when s is a bf16 tie (low half 0x8000), and
+// there the sign of e decides: the exact sum is farther from zero than s when
+// e has s's sign (round the magnitude up), else nearer (truncate).
+__device__ __forceinline__ uint16_t sum_to_bf16(float a, float b) {
+  const float s = a + b;
+  const uint32_t u = __float_as_uint(s);
+  if ((u & 0xFFFFu) != 0x8000u || (u & 0x7F800000u) == 0x7F800000u) return f32_to_bf16(s);
+  const float bb = s - a;
+  const float e = (a - (s - bb)) + (b - bb);
+  if (e == 0.f) return f32_to_bf16(s);
+  return (uint16_t)((u >> 16) + (((e > 0.f) == (s > 0.f)) ? 1u : 0u));
+}
+
 template <typename T>
 struct Elem;
 template <>
@@ -44,12 +59,15 @@ struct Elem<bf16_t> {
   static constexpr int kBytes = 2;
   __device__ static float to_f32(const void* base, size_t i) { return bf16_to_f32(((const uint16_t*)base)[i]); }
   __device__ static void store(void* base, size_t i, float v) { ((uint16_t*)base)[i] = f32_to_bf16(v); }
+  // round(a + b) of the exact sum
+  __device__ static void store_sum(void* base, size_t i, float a, float b) { ((uint16_t*)base)[i] = sum_to_bf16(a, b); }
 };
 template <>
 struct Elem<float> {
   static constexpr int kBytes = 4;
   __device__ static float to_f32(const void* base, size_t i) { return ((const float*)base)[i]; }
   __device__ static void store(void* base, size_t i, float v) { ((float*)base)[i] = v; }
+  __device__ static void store_sum(void* base, size_t i, float a, float b) { ((float*)base)[i] = a + b; }
 };
 
 // 16-byte global load (the address must be 16-byte aligned).
@@ -232,7 +250,23 @@ __device__ __forceinline__ f32x4 ld_dev4(const float* p) {
                __uint_as_float((uint32_t)(hi >> 32))};
 }
 // Wait until this wave's memory operations have completed (stores acknowledged).
-__device__ __forceinline__ void stores_done() { __builtin_amdgcn_s_waitcnt(0); }
+// The signal fences keep the compiler from moving memory operations across the
+// wait (they emit no instruction).
+__device__ __forceinline__ void stores_done() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// Completion ticket: an agent-scope release read-modify-write.  Every store of
+// this workgroup that happens before it (this wave's own, and the other waves'
+// through the workgroup barrier before it) is ordered before the new count, and
+// the counter's read-modify-writes form one release sequence, so the workgroup
+// that reads the final count and then takes acquire_agent() sees all of them.
+__device__ __forceinline__ int32_t ticket_release(int32_t* p) {
+  return __hip_atomic_fetch_add(p, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void acquire_agent() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
 
 // Intra-wave ordering point for LDS data written and read by the same wave.
 __device__ __forceinline__ void wave_lds_sync() {

@@ -23,7 +23,8 @@ struct AttnArgs {
   float* part_o;           // [B*Hkv*n_rowblk][nsplit][rows_per_wg][D] unnormalised split outputs
   float* part_m;           // [B*Hkv*n_rowblk][nsplit][rows_per_wg]   (log2 units)
   float* part_l;
-  void* x_out;             // [M][Hd] residual h + O in the workload dtype
+  void* x_out;             // [M][Hd] residual h + O in the workload dtype (workspace, the LM head's input)
+  void* x_copy;            // [M][Hd] the caller's copy of x, or null
   float* attn_out;         // [M][Hd] or null
   int32_t total_nodes, hidden_size, n_kv_heads, group, kv_cap, max_nodes;
   int32_t nsplit, chunk, n_rowblk, rows_per_wg, wr, wk;
@@ -63,6 +64,18 @@ struct VocabArgs {
   int32_t total_nodes, batch, vocab, n_vtiles, topk_out, max_nodes, max_depth, kv_cap, max_kv;
   int32_t topk, min_lookahead, max_relaxed;
   float tau;
+  int32_t stats_only;      // 1: rows write their flags and stop (no ticket, no path reduction)
+  int32_t* rank_req;       // [M] workspace: parent row of node i whose rank the rank pass counts, or -1;
+                           // null when tok_rank is not requested
+  int32_t* tok_rank;       // [M] output, set to 0 (counted by the rank pass) or -1 here; null: not requested
+};
+
+struct RankArgs {
+  const float* logits;     // [M][V]
+  const int32_t* token;    // [M]
+  const int32_t* rank_req; // [M] parent row of node j, or -1 (written by the vocabulary pass)
+  int32_t* tok_rank;       // [M] zeroed (or -1) by the vocabulary pass; the counts are added here
+  int32_t total_nodes, vocab;
 };
 
 struct StochArgs {
@@ -125,6 +138,9 @@ constexpr int kLmTileRows = 64;  // vocabulary rows per LM-head workgroup (one s
 constexpr int kTileWords = 4;
 hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
 hipError_t launch_stochastic(const StochArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
+// exact ranks of the children's tokens (after the vocabulary pass); chunks of kRankChunk tokens
+constexpr int kRankChunk = 4096;
+hipError_t launch_rank(const RankArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
 constexpr int kMaxStochVocab = 256 * 2048;  // the draw's per-tile masses: 256 tiles of 2048 tokens
 hipError_t launch_zero_i32(int32_t* p, size_t n, hipStream_t s);
 

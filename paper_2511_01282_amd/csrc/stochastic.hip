@@ -417,9 +417,10 @@ __global__ __launch_bounds__(kST) void stochastic_kernel(StochArgs a) {
   }
   stores_done();
   __syncthreads();
-  if (tid == 0) sh.ticket = atomicAdd(a.seq_counter + b, 1);
+  if (tid == 0) sh.ticket = ticket_release(a.seq_counter + b);
   __syncthreads();
   if (sh.ticket != n - 1 || wave != 0) return;
+  acquire_agent();  // the other rows' hand-off words are read after their release
 
   // ---- the walk (one wave, last row of the sequence) ----
   for (int j = lane; j < kMaxNodes; j += 64) {

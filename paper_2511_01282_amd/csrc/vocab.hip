@@ -477,6 +477,12 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
     c_src[u] = a.src[jn];
   }
   const int kv_b = a.kv_len[lay_ok ? b : 0];
+  // node i's own parent and token: the rank pass counts node i's token in its parent's row
+  int my_par = -1, my_tok = -1;
+  if (a.rank_req) {
+    my_par = a.parent[i];
+    my_tok = a.token[i];
+  }
 
   // Fold the row's tile statistics (this thread's tiles), and keep each tile's
   // largest (value, id) key; the id's tile is the tile.
@@ -635,6 +641,11 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
     __syncthreads();
   else
     wave_lds_sync();
+  if (a.rank_req && tid == 0) {
+    const bool rq = lay_ok && li > 0 && my_par >= 0 && my_par < li && my_tok >= 0 && my_tok < a.vocab;
+    a.rank_req[i] = rq ? n0 + my_par : -1;
+    a.tok_rank[i] = rq ? 0 : -1;
+  }
   if (!lay_ok) return;  // uniform over the workgroup
 
   // predicates of the children of node li: thread j describes node j (and j + NT)
@@ -658,25 +669,33 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
     }
     st_dev(a.flag_ws + n0 + j, (int32_t)f);
     a.tok_logprob[n0 + j] = lp;
+    if (a.stats_only) a.flags[n0 + j] = (uint8_t)f;
   }
   if (li == 0 && tid == 0) {
     st_dev(a.flag_ws + n0, 0);
     a.tok_logprob[n0] = 0.f;
+    if (a.stats_only) a.flags[n0] = 0;
   }
+  if (a.stats_only) return;  // (uniform) statistics and predicates only
 
   // tree checks and leaf chains (wave 0) while the stores drain
   PathPrep pp{};
   if (wave == 0) pp = path_prepare(a, n, sh.par, sh.tok, sh.src, sh.hc, sh.chain, lane);
 
   // ---- sequence completion ticket ----
+  // Every wave's hand-off stores are complete before the workgroup barrier; the
+  // ticket is an agent-scope release RMW (it orders them before the count), and
+  // the winner, which reads the count of every other row, takes an agent-scope
+  // acquire before it reads their hand-off words.
   stores_done();
   if constexpr (WPR > 1) __syncthreads();
-  if (tid == 0) sh.ticket = atomicAdd(a.seq_counter + b, 1);
+  if (tid == 0) sh.ticket = ticket_release(a.seq_counter + b);
   if constexpr (WPR > 1)
     __syncthreads();
   else
     wave_lds_sync();
   if (sh.ticket != n - 1 || wave != 0) return;
+  acquire_agent();
   path_finish(a, b, n0, n, kv_b, pp, sh.par, sh.flag, sh.node_am, sh.chain, lane);
   if (lane == 0) st_dev(a.seq_counter + b, 0);
 }
@@ -717,6 +736,42 @@ hipError_t launch_finalize(int ko, int blocks, const VocabArgs& a, hipStream_t s
   if (ko == 8) return launch_finalize_ko<8>(blocks, a, s, ev_stop);
   if (ko == 16) return launch_finalize_ko<16>(blocks, a, s, ev_stop);
   return hipErrorInvalidValue;
+}
+
+// Exact rank of node j's token t in its parent's logit row z (float32, as the
+// vocabulary pass leaves them): #{u : z_u > z_t} + #{u < t : z_u == z_t}.
+// Workgroup (c, j) counts over tokens [c*kRankChunk, (c+1)*kRankChunk) and adds
+// its count to tok_rank[j] (zeroed by the vocabulary pass when j has a request).
+__global__ __launch_bounds__(256) void rank_kernel(RankArgs a) {
+  const int j = blockIdx.y;
+  const int row = a.rank_req[j];  // (uniform) parent row, or -1: no rank for node j
+  if (row < 0 || row >= a.total_nodes) return;
+  const int t = a.token[j];
+  if (t < 0 || t >= a.vocab) return;
+  const float* zr = a.logits + (size_t)row * a.vocab;
+  const float zt = zr[t];
+  const int u0 = blockIdx.x * kRankChunk;
+  int cnt = 0;
+#pragma unroll
+  for (int k = 0; k < kRankChunk / 256; ++k) {
+    const int u = u0 + k * 256 + (int)threadIdx.x;
+    const float z = u < a.vocab ? zr[u] : kNegInf;
+    cnt += (u < a.vocab && (z > zt || (z == zt && u < t))) ? 1 : 0;
+  }
+  for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+  __shared__ int s_cnt[4];
+  if ((threadIdx.x & 63) == 0) s_cnt[threadIdx.x >> 6] = cnt;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int total = s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
+    if (total) atomicAdd(a.tok_rank + j, total);
+  }
+}
+
+hipError_t launch_rank(const RankArgs& a, hipStream_t s, hipEvent_t ev_stop) {
+  if (a.total_nodes <= 0) return hipSuccess;
+  const dim3 grid((a.vocab + kRankChunk - 1) / kRankChunk, a.total_nodes);
+  return launch_k(rank_kernel, grid, dim3(256), 0, s, nullptr, ev_stop, a);
 }
 
 __global__ void zero_i32_kernel(int32_t* p, size_t n) {

@@ -59,20 +59,31 @@ def step_kwargs(w, params=None) -> dict:
 
 
 def run(w, *, plan=None, inputs=None, params=None, stop_after=binding.STOP_ALL, attn_out=True,
-        device="cuda", repeat=1, step_kw=None) -> dict:
+        device="cuda", repeat=1, step_kw=None, x_out=False, tok_rank=False) -> dict:
     """One (or ``repeat``) steps; returns every output as numpy arrays.
 
-    ``step_kw`` overrides the host-side step arguments derived from ``w``.
+    ``step_kw`` overrides the host-side step arguments derived from ``w``; ``x_out`` and
+    ``tok_rank`` also request the residual x (as the workload's bit patterns: uint16 for
+    bf16) and the draft tokens' exact ranks.
     """
     kw = step_kwargs(w, params)
     kw.update(step_kw or {})
     plan = plan or make_plan(w, device, max_kv_len=kw["max_kv_len_in_batch"])
     inputs = inputs or upload(w, device)
     s = w.shape
+    xd = (torch.bfloat16 if s.dtype == "bf16" else torch.float32) if x_out else None
     out = binding.alloc_outputs(total_nodes=kw["total_nodes"], batch=kw["batch"], hidden=s.hidden,
                                 vocab=s.vocab, topk_out=s.topk_out, max_depth=s.max_depth, device=device,
-                                attn_out=attn_out)
+                                attn_out=attn_out, x_dtype=xd, tok_rank=tok_rank)
     for _ in range(repeat):
         plan.step(inputs, out, stop_after=stop_after, **kw)
     torch.cuda.synchronize(device)
-    return {k: (v.cpu().numpy() if v is not None else None) for k, v in out.items()}
+    res = {}
+    for k, v in out.items():
+        if v is None:
+            res[k] = None
+        elif v.dtype == torch.bfloat16:
+            res[k] = v.view(torch.int16).cpu().numpy().view(np.uint16)
+        else:
+            res[k] = v.cpu().numpy()
+    return res

@@ -110,7 +110,7 @@ def _args(b, **over):
 
 
 @pytest.mark.parametrize("over,code", [
-    (dict(stop_after=3), 4), (dict(batch=-1), 2), (dict(batch=2), 6),
+    (dict(stop_after=4), 4), (dict(stop_after=-1), 4), (dict(batch=-1), 2), (dict(batch=2), 6),
     (dict(topk=0), 4), (dict(topk=9), 4), (dict(tau=-1.0), 4), (dict(tau=float("nan")), 4),
     (dict(tau=float("inf")), 4), (dict(min_lookahead=-1), 4), (dict(max_relaxed=-1), 4),
     (dict(max_nodes_in_batch=0), 2), (dict(max_nodes_in_batch=27), 6), (dict(max_kv_len_in_batch=4096), 6),
@@ -150,6 +150,42 @@ def test_attention_only_step_needs_no_logit_buffers(b):
     a = _args(b, stop_after=1, lm_head=None, logits=None, topk=0, kv_capacity=10)
     assert b.lib().respec_verify_step(h, ctypes.byref(a), FAKE, None) == 2
     b.lib().respec_verify_destroy(h)
+
+
+def test_statistics_only_step_needs_no_path_buffers(b):
+    # stop_after = STATS: the path outputs may be NULL (the alignment check after the
+    # NULL checks then fails, so nothing is launched), but the statistics and flags may not
+    _, h = _create(b, _shape(b))
+    none = dict(leaf_acc_len=None, path=None, acc_len=None, bonus=None, winner_leaf=None, seq_status=None,
+                sample=None, hidden=FAKE + 8)
+    a = _args(b, stop_after=3, **none)
+    assert b.lib().respec_verify_step(h, ctypes.byref(a), FAKE, None) == 2
+    for f in ("flags", "entropy", "topk_id", "token"):
+        a = _args(b, stop_after=3, **dict(none, **{f: None}))
+        assert b.lib().respec_verify_step(h, ctypes.byref(a), FAKE, None) == 1, f
+    # the statistics level still checks the acceptance parameters (the predicates use them)
+    a = _args(b, stop_after=3, topk=0)
+    assert b.lib().respec_verify_step(h, ctypes.byref(a), FAKE, None) == 4
+    b.lib().respec_verify_destroy(h)
+
+
+def test_noalloc_step_checks_before_any_device_call(b):
+    L = b.lib()
+    a = _args(b)
+    assert L.respec_verify_step_noalloc(None, ctypes.byref(a), None) == 1
+    _, h = _create(b, _shape(b))
+    assert L.respec_verify_step_noalloc(h, None, None) == 1
+    L.respec_verify_destroy(h)
+    # a plan whose workspace exceeds the static scratch is refused on the host
+    _, big = _create(b, _shape(b, max_batch=64, max_nodes=128, max_kv_len=32768, vocab=128256, n_kv_heads=8))
+    assert L.respec_verify_workspace_bytes(big) > b.NOALLOC_SCRATCH_BYTES
+    assert L.respec_verify_step_noalloc(big, ctypes.byref(a), None) == b.ERR_SCRATCH
+    L.respec_verify_destroy(big)
+    st, many = _create(b, _shape(b, max_batch=b.NOALLOC_MAX_BATCH + 1, max_nodes=1, max_kv_len=16, vocab=64,
+                                 hidden=256, n_q_heads=2, n_kv_heads=2))
+    assert st == 0
+    assert L.respec_verify_step_noalloc(many, ctypes.byref(a), None) == b.ERR_SCRATCH
+    L.respec_verify_destroy(many)
 
 
 def test_empty_batch_is_a_no_op(b):

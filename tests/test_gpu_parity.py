@@ -10,6 +10,18 @@ Same seeded inputs on both sides.  Bar:
     workloads additionally within 1e-4.
 Every workload keeps acceptance decisions >= 1e-3 away from their thresholds
 (see tests/workload.py), so the float differences cannot flip a decision.
+
+The residual x = round(h + O) that feeds the LM head is compared bit for bit
+(bf16) against the oracle's, which rounds the exact sum once: where they
+differ, the GPU's value must still be the rounding of a sum within X_EPS of
+the oracle's exact sum (the kernel's O differs from the oracle's by far less
+than X_EPS), i.e. lie between round(pre - X_EPS) and round(pre + X_EPS).
+That happens only next to a rounding midpoint, or for sums so close to zero
+that bf16's spacing there is below X_EPS.
+tok_rank is compared exactly wherever the oracle's logits are unambiguous
+(no other logit within RANK_EPS, the logit tolerance, of the token's); where
+one is, the GPU's rank must lie in the range those logits allow.  It must
+also be exactly the rank of the token in the logits the GPU returned.
 """
 import numpy as np
 import pytest
@@ -20,6 +32,8 @@ import workload
 pytestmark = pytest.mark.gpu
 
 RTOL, ATOL = 2e-2, 1e-3
+X_EPS = 1e-5      # bound on |O_gpu - O_oracle| (measured: < 1e-6) within which x may round either way
+RANK_EPS = ATOL   # logits this close to the token's may order either way
 
 
 @pytest.fixture(scope="module")
@@ -37,32 +51,100 @@ def _say(msg):
 
 
 def compare(case, out, label, check_float=True):
+    # rows of sequences reported as malformed carry no defined values (the oracle gives
+    # their nodes a stand-in ancestor set): only the integer outputs are compared there
     e = case.expected
     w = case.w
     z32 = case.z.astype(np.float32)
+    valid = e["seq_status"][_seq_of(w)] == 0
     if check_float:
         if out.get("attn_out") is not None:
-            err = np.abs(out["attn_out"] - case.attn).max()
+            err = np.abs(out["attn_out"][valid] - case.attn[valid]).max()
             _say(f"[{label}] max|dO| = {err:.3e}")
-            np.testing.assert_allclose(out["attn_out"], case.attn, rtol=RTOL, atol=ATOL)
-        err = np.abs(out["logits"] - case.z).max()
+            np.testing.assert_allclose(out["attn_out"][valid], case.attn[valid], rtol=RTOL, atol=ATOL)
+        err = np.abs(out["logits"][valid] - case.z[valid]).max()
         _say(f"[{label}] max|dz| = {err:.3e}")
-        np.testing.assert_allclose(out["logits"], case.z, rtol=RTOL, atol=ATOL)
+        np.testing.assert_allclose(out["logits"][valid], case.z[valid], rtol=RTOL, atol=ATOL)
         for k in ("max_logit", "lse", "entropy"):
-            np.testing.assert_allclose(out[k], e[k], rtol=RTOL, atol=ATOL, err_msg=k)
-        np.testing.assert_allclose(out["topk_logprob"], e["topk_logprob"], rtol=RTOL, atol=ATOL)
-        valid = e["seq_status"][_seq_of(w)] == 0
+            np.testing.assert_allclose(out[k][valid], e[k][valid], rtol=RTOL, atol=ATOL, err_msg=k)
+        np.testing.assert_allclose(out["topk_logprob"][valid], e["topk_logprob"][valid], rtol=RTOL, atol=ATOL)
         nonroot = np.array([w.parent[j] >= 0 for j in range(len(w.parent))]) & valid
         np.testing.assert_allclose(out["tok_logprob"][nonroot], e["tok_logprob"][nonroot], rtol=RTOL, atol=ATOL)
         if w.shape.dtype == "f32":
-            np.testing.assert_allclose(out["logits"], case.z, rtol=1e-4, atol=1e-4)
-            np.testing.assert_allclose(out["entropy"], e["entropy"], rtol=1e-4, atol=1e-4)
-    np.testing.assert_array_equal(out["argmax"], e["argmax"], err_msg="argmax")
+            np.testing.assert_allclose(out["logits"][valid], case.z[valid], rtol=1e-4, atol=1e-4)
+            np.testing.assert_allclose(out["entropy"][valid], e["entropy"][valid], rtol=1e-4, atol=1e-4)
+    np.testing.assert_array_equal(out["argmax"][valid], e["argmax"][valid], err_msg="argmax")
     gid, oid = out["topk_id"], e["topk_id"]
-    for r, k in zip(*np.nonzero(gid != oid)):
+    for r, k in zip(*np.nonzero((gid != oid) & valid[:, None])):
         assert abs(float(z32[r, gid[r, k]]) - float(z32[r, oid[r, k]])) < 1e-4, (r, k)
     for name in ("flags", "leaf_acc_len", "path", "acc_len", "bonus", "winner_leaf", "seq_status"):
         np.testing.assert_array_equal(out[name], e[name], err_msg=name)
+    if out.get("x_out") is not None:
+        check_x(case, out["x_out"], label, valid)
+    if out.get("tok_rank") is not None:
+        check_rank(case, out["tok_rank"], out["logits"], label)
+
+
+def check_x(case, x_out, label, valid=None):
+    """x against the oracle's residual: bit-exact for bf16 up to near-midpoint sums."""
+    w = case.w
+    if valid is None:
+        valid = np.ones(x_out.shape[0], bool)
+    if w.shape.dtype != "bf16":
+        np.testing.assert_allclose(x_out[valid].astype(np.float64), case.x[valid], rtol=1e-4, atol=1e-4,
+                                   err_msg="x")
+        return
+    gpu = synth.bf16_bits_to_f32(x_out).astype(np.float64)
+    diff = (gpu != case.x) & valid[:, None]
+    n = int(diff.sum())
+    if n:
+        pre = (synth.bf16_bits_to_f32(w.hidden).astype(np.float64) + case.attn)[diff]
+        lo, hi = _rne_bf16(pre - X_EPS), _rne_bf16(pre + X_EPS)
+        g = gpu[diff]
+        bad = (g < lo) | (g > hi)
+        assert not bad.any(), (f"x differs at {int(bad.sum())} elements by more than a rounding of a sum "
+                               f"within {X_EPS} of the exact one: gpu {g[bad][:4]}, oracle {case.x[diff][bad][:4]}, "
+                               f"exact sum {pre[bad][:4]}")
+    _say(f"[{label}] x bit-exact at {int(valid.sum()) * x_out.shape[1] - n} of {int(valid.sum()) * x_out.shape[1]} "
+         f"elements ({n} sums within {X_EPS} of a rounding boundary)")
+
+
+def _rne_bf16(d):
+    """Nearest bf16 value (ties to even) of doubles d: d = m 2^e, spacing 2^(e-8)."""
+    m, e = np.frexp(d)
+    q = np.ldexp(1.0, np.maximum(e - 8, -133))
+    return np.where(d == 0, 0.0, np.rint(d / q) * q)
+
+
+def check_rank(case, rank, logits, label):
+    """tok_rank: exact where the oracle's logits order the token unambiguously, else in range."""
+    w, e = case.w, case.expected
+    seq = _seq_of(w)
+    z = case.z
+    n_exact = n_range = 0
+    for j in range(len(w.parent)):
+        b = seq[j]
+        if e["seq_status"][b] != 0 or w.parent[j] < 0:
+            continue
+        i = int(w.node_off[b]) + int(w.parent[j])
+        t = int(w.token[j])
+        zi, zt = z[i], z[i, t]
+        lo = int((zi > zt + RANK_EPS).sum())
+        hi = int((zi >= zt - RANK_EPS).sum()) - 1
+        assert lo <= int(e["tok_rank"][j]) <= hi
+        if lo == hi:
+            assert rank[j] == e["tok_rank"][j], (label, j, rank[j], e["tok_rank"][j])
+            n_exact += 1
+        else:
+            assert lo <= rank[j] <= hi, (label, j, rank[j], lo, hi)
+            n_range += 1
+        # the rank of the token in the logits the GPU returned
+        g = logits[i]
+        gt = g[t]
+        assert rank[j] == int((g > gt).sum()) + int(((g == gt) & (np.arange(g.shape[0]) < t)).sum())
+    roots = w.parent < 0
+    assert (rank[roots] == -1).all()
+    _say(f"[{label}] tok_rank exact at {n_exact} nodes, within the logit tolerance at {n_range}")
 
 
 def _seq_of(w):
@@ -82,7 +164,7 @@ def test_config_parity(rt, cfg):
     _say(f"[config {cfg}] building case (seed {synth.SEED_BASE + cfg})")
     case = workload.build(cfg)
     _say(f"[config {cfg}] running GPU step: acc_len={case.expected['acc_len'].tolist()}")
-    out = rt.run(case.w)
+    out = rt.run(case.w, x_out=True, tok_rank=True)
     compare(case, out, f"config {cfg}")
 
 
@@ -130,7 +212,7 @@ def test_edge_case_parity(rt, name):
     _say(f"[edge {name}] building")
     case = workload.finish(w)
     _say(f"[edge {name}] running GPU step")
-    compare(case, rt.run(case.w), f"edge {name}")
+    compare(case, rt.run(case.w, x_out=True, tok_rank=True), f"edge {name}")
 
 
 # Vocabulary sizes that take each form of the vocabulary pass: one wave per row
@@ -173,7 +255,7 @@ def test_vocab_tier_parity(rt, vocab, topk_out, mode):
     _say(f"[vocab {vocab} k={topk_out} {mode}] building")
     case = workload.finish(w)
     _say(f"[vocab {vocab} k={topk_out} {mode}] running GPU step")
-    compare(case, rt.run(case.w), f"vocab {vocab}")
+    compare(case, rt.run(case.w, tok_rank=True), f"vocab {vocab}")
 
 
 def _depth(parent):
@@ -213,6 +295,24 @@ def test_stop_after_stages(rt):
 
 
 @pytest.mark.timeout(300)
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_stop_after_statistics(rt, cfg):
+    # statistics and predicates only: the same values as the whole step, flags without
+    # ON_PATH, and no path reduction (its outputs keep what they held)
+    from paper_2511_01282_amd import binding
+    case = workload.build(cfg)
+    e = case.expected
+    _say(f"[stop_after] statistics, config {cfg}")
+    out = rt.run(case.w, stop_after=binding.STOP_STATS, tok_rank=True, x_out=True)
+    for k in ("max_logit", "lse", "entropy", "topk_logprob"):
+        np.testing.assert_allclose(out[k], e[k], rtol=RTOL, atol=ATOL, err_msg=k)
+    np.testing.assert_array_equal(out["argmax"], e["argmax"])
+    np.testing.assert_array_equal(out["flags"], e["flags"] & np.uint8(15))
+    check_x(case, out["x_out"], f"stats {cfg}")
+    check_rank(case, out["tok_rank"], out["logits"], f"stats {cfg}")
+
+
+@pytest.mark.timeout(300)
 def test_repeated_steps_are_bitwise_identical(rt):
     case = workload.build(1)
     plan = rt.make_plan(case.w)
@@ -224,6 +324,55 @@ def test_repeated_steps_are_bitwise_identical(rt):
             if v is not None:
                 np.testing.assert_array_equal(v, outs[0][k], err_msg=k)
     compare(case, outs[-1], "repeat")
+
+
+def _wide_batch(n_seq=70, seed=401):
+    """n_seq small ragged trees (1-7 nodes, prefixes of 0-150 rows): a batch past 64 sequences."""
+    u = synth.uniform_stream(seed, 90, 0, 4 * n_seq + 200)
+    parents, kv = [], []
+    for s in range(n_seq):
+        n = 1 + int(u[s] * 7)
+        parents.append([-1] + [int(u[n_seq + s * 3 + k % 3] * k) for k in range(1, n)])
+        kv.append(int(u[3 * n_seq + s] * 151))
+    # the cache holds the longest prefix plus the largest tree: give the longest prefix a 7-node tree
+    longest = int(np.argmax(kv))
+    parents[longest] = [-1, 0, 1, 1, 3, 0, 5]
+    return parents, kv
+
+
+@pytest.mark.timeout(300)
+def test_wide_batch_parity(rt):
+    # 70 sequences: the register-path attention with per-sequence splits, the vocabulary
+    # pass's node-offset scan over several groups of 64; sequence 13 has a malformed tree
+    parents, kv = _wide_batch()
+    parents[13] = [-1, 0, 2]                 # node 2 is its own parent
+    shp = synth.Shape("edge", "bf16", 4 * 64, 4, 2, 64, 3000, len(parents), 7, 8, 8)
+    w = synth.custom(shp, parents, kv, seed=402, poison_tail=True)
+    _say("[wide batch] building 70 sequences")
+    case = workload.finish(w)
+    assert case.expected["seq_status"][13] == 5 and (case.expected["seq_status"] == 0).sum() == 69
+    _say("[wide batch] running GPU step")
+    compare(case, rt.run(case.w, x_out=True, tok_rank=True), "wide batch")
+
+
+@pytest.mark.timeout(300)
+def test_wide_batch_with_broken_node_offsets(rt):
+    # one empty node range among 70: the offsets no longer describe the batch, so every
+    # sequence is reported as a malformed tree (and nothing reads outside the buffers)
+    parents, kv = _wide_batch(seed=403)
+    shp = synth.Shape("edge", "bf16", 4 * 64, 4, 2, 64, 3000, len(parents), 7, 8, 8)
+    w = synth.custom(shp, parents, kv, seed=404, poison_tail=True)
+    case = workload.finish(w)
+    bad = case.w
+    w = synth.custom(shp, parents, kv, seed=404, poison_tail=True)
+    bad.node_off = bad.node_off.copy()
+    bad.node_off[40] = bad.node_off[41]      # sequence 40 empty, sequence 39 longer
+    _say("[wide batch] running GPU step with an empty node range")
+    # (the host arguments describe the real batch; only the device offsets are broken)
+    out = rt.run(bad, step_kw=dict(max_nodes_in_batch=int(np.diff(w.node_off).max())))
+    assert (out["seq_status"] == 5).all()
+    assert (out["acc_len"] == -1).all() and (out["path"] == -1).all()
+    assert (out["winner_leaf"] == -1).all() and (out["bonus"] == -1).all()
 
 
 def test_invalid_device_data_is_reported_per_sequence(rt):
