@@ -74,20 +74,6 @@ static double load(int32_t dtype, const void* base, int64_t i) {
     return (double)((const float*)base)[i];
 }
 
-/* Round a float32 to bf16, round-to-nearest-even on the bit pattern. */
-static float round_bf16(float f) {
-    uint32_t u;
-    memcpy(&u, &f, 4);
-    if ((u & 0x7F800000u) == 0x7F800000u) { /* inf / nan: keep, quiet the nan */
-        if (u & 0x007FFFFFu) u |= 0x00400000u;
-        u &= 0xFFFF0000u;
-    } else {
-        u = (u + 0x7FFFu + ((u >> 16) & 1u)) & 0xFFFF0000u;
-    }
-    memcpy(&f, &u, 4);
-    return f;
-}
-
 /* ------------------------------------------------------------------------ */
 /* Tree (Algorithm 1, BuildDraftTree / RelaxedVerify; Section 3.5).
  * parent[0] = -1 marks the root; every other node's parent precedes it.
@@ -180,17 +166,29 @@ void respec_oracle_attention(int32_t dtype, const void* hidden, int32_t hidden_s
 }
 
 /* ------------------------------------------------------------------------ */
-/* Residual and rounding point of the one-layer proxy: x = round(h + O).
- * O is first rounded to float32 and added to h in float32, then rounded to
- * the workload dtype -- the same precision the GPU takes this decision in.
- * x is returned widened to double (exactly representable).                 */
+/* Round d to the nearest number with `sig` significant bits, ties to even:
+ * d = m 2^e with 1/2 <= |m| < 1, so the spacing of such numbers at d is
+ * 2^(e - sig); below the normal range the spacing stays 2^min_exp.  d / q and
+ * rint(.) q are exact, and rint rounds half to even.  float32 is (24, -149),
+ * bf16 (8, -133); the values here stay far inside both ranges.             */
+static double round_sig(double d, int sig, int min_exp) {
+    if (d == 0.0 || !isfinite(d)) return d;
+    int e;
+    frexp(d, &e);
+    int qe = e - sig;
+    if (qe < min_exp) qe = min_exp;
+    double q = ldexp(1.0, qe);
+    return rint(d / q) * q;
+}
+
+/* Residual and rounding point of the one-layer proxy: x = round(h + O), the
+ * exact sum h + O (in double) rounded once to the workload dtype, round to
+ * nearest even.  x is returned widened to double (exactly representable).  */
 void respec_oracle_residual(int32_t dtype, const void* hidden, const double* attn,
                             int64_t count, double* x) {
     for (int64_t i = 0; i < count; ++i) {
-        float h = (float)load(dtype, hidden, i);
-        float o = (float)attn[i];
-        float s = h + o;
-        x[i] = (double)(dtype == ORACLE_BF16 ? round_bf16(s) : s);
+        double s = load(dtype, hidden, i) + attn[i];
+        x[i] = dtype == ORACLE_BF16 ? round_sig(s, 8, -133) : round_sig(s, 24, -149);
     }
 }
 

@@ -57,11 +57,20 @@ class _OracleSession:
 
 
 def _gpu_verify(m):
+    # Every step's decisions (argmax gaps, tau and rank-k boundaries) must sit at
+    # least MARGIN away from their thresholds in the oracle's logits of that step,
+    # so float32 differences between the two paths cannot flip one: a near-tie is
+    # reported as such instead of surfacing as a divergence of the loops.
+    import workload
     from paper_2511_01282_amd import runner
     plan = runner.make_plan(dl.workload(m, [0, 0], [-1], [0], [0]), "cuda:0", max_nodes=m.shape.max_nodes,
                             max_kv_len=4096)
+    count = [0]
 
     def verify(w):
+        margin = workload.min_decision_margin(w, oracle.forward(w)["z"])
+        assert margin >= workload.MARGIN, f"step {count[0]}: a decision is {margin:.2e} from its threshold"
+        count[0] += 1
         return runner.run(w, plan=plan, device="cuda:0", attn_out=False)
     return verify
 

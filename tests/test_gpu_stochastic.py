@@ -32,6 +32,7 @@ CASES = {
     "c0-T1": (0, 1.0, True),
     "c1-T0.7": (1, 0.7, True),
     "c1-deterministic-T1.3": (1, 1.3, False),
+    "c2-T1": (2, 1.0, True),
     "c3-T1": (3, 1.0, True),
     "c4-T1": (4, 1.0, True),
     "star30-T1.5": ("star", 1.5, True),

@@ -159,15 +159,36 @@ def test_gqa_equals_mha_with_replicated_heads():
 # residual, logits
 # ---------------------------------------------------------------------------
 
-def test_residual_rounds_like_torch_bf16():
+def _nearest_bf16(d: float) -> float:
+    """Brute force: the bf16 value nearest to d, ties to the even bit pattern."""
+    b0 = int(np.array([d], np.float32).view(np.uint32)[0]) >> 16
+    cands = [b for b in range(b0 - 2, b0 + 3) if 0 <= b < 0x10000]
+    vals = [(abs(float(np.array([b << 16], np.uint32).view(np.float32)[0]) - d), b & 1, b) for b in cands]
+    best = min(vals)
+    return float(np.array([best[2] << 16], np.uint32).view(np.float32)[0])
+
+
+def test_residual_rounds_the_exact_sum_once_to_bf16():
+    # x = RNE_bf16(h + O) of the exact (double) sum.  Besides random sums: exact
+    # midpoints between neighbouring bf16 values (ties go to the even pattern) and
+    # sums a hair above or below a midpoint, which a float32 sum would first round
+    # onto the midpoint (rounding twice then goes the wrong way on half of them).
     rng = np.random.default_rng(0)
-    h32 = rng.standard_normal(4096).astype(np.float32)
-    hb = synth.f32_to_bf16_bits(h32)
+    hb = synth.f32_to_bf16_bits(rng.standard_normal(4096).astype(np.float32))
+    h = synth.bf16_bits_to_f32(hb).astype(np.float64)
     o = rng.standard_normal(4096) * 0.05
+    up = (hb.astype(np.uint32) + 1).astype(np.uint16)
+    mid = (h + synth.bf16_bits_to_f32(up).astype(np.float64)) / 2
+    o[:1024] = mid[:1024] - h[:1024]                          # exact ties
+    o[1024:2048] = mid[1024:2048] - h[1024:2048] + np.abs(h[1024:2048]) * 2.0 ** -40
+    o[2048:3072] = mid[2048:3072] - h[2048:3072] - np.abs(h[2048:3072]) * 2.0 ** -40
     x = oracle.residual(oracle.BF16, hb, o)
-    hf = torch.from_numpy(synth.bf16_bits_to_f32(hb).copy())
-    ref = (hf + torch.from_numpy(o).to(torch.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    ref = np.array([_nearest_bf16(float(a) + float(b)) for a, b in zip(h, o)])
     np.testing.assert_array_equal(x, ref)
+    # and in float32 workloads, numpy's round-to-nearest-even cast of the double sum
+    hf = rng.standard_normal(4096).astype(np.float32)
+    x32 = oracle.residual(oracle.F32, hf, o)
+    np.testing.assert_array_equal(x32, (hf.astype(np.float64) + o).astype(np.float32).astype(np.float64))
 
 
 def test_logits_match_library_gemm():

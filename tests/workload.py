@@ -46,6 +46,33 @@ def _token_ok(row32: np.ndarray, order: np.ndarray, t: int, amax: int, k: int, t
     return float(row32[order[k - 1]]) - zt >= MARGIN
 
 
+def min_decision_margin(w, z) -> float:
+    """Smallest distance of any decision of step ``w`` (oracle logits ``z``) from its threshold:
+    every row's top-1 / top-2 gap (argmax, the bonus token) and, for every non-greedy draft
+    token, its distance from the tau boundary and from the rank-k boundary."""
+    p = w.params
+    z32 = np.asarray(z, np.float32)
+    m = np.inf
+    for b in range(len(w.node_off) - 1):
+        lo, hi = int(w.node_off[b]), int(w.node_off[b + 1])
+        for i in range(lo, hi):
+            top2 = np.partition(z32[i], -2)[-2:]
+            m = min(m, float(top2[1]) - float(top2[0]))
+        for j in range(lo + 1, hi):
+            i = lo + int(w.parent[j])
+            row, t = z32[i], int(w.token[j])
+            order = _order(row)
+            a = int(order[0])
+            if t == a:
+                continue
+            zt, za = float(row[t]), float(row[a])
+            m = min(m, abs((za - zt) - p.tau))
+            r = int(np.nonzero(order == t)[0][0])
+            if p.topk < row.shape[0]:
+                m = min(m, zt - float(row[order[p.topk]]) if r < p.topk else float(row[order[p.topk - 1]]) - zt)
+    return m
+
+
 def _order(row32: np.ndarray) -> np.ndarray:
     ids = np.arange(row32.shape[0])
     return np.lexsort((ids, -row32.astype(np.float64)))
