@@ -13,8 +13,11 @@ that the working set exceeds the 256 MB Infinity Cache and every step streams
 its bytes from HBM.  The timed region runs K plain steps.  A second pass of K
 steps records HIP events on the step's stream around each stage (attention
 with its split merge, LM head, vocabulary pass); they give each stage's
-average duration for the roofline figures.  The CPU baseline times the oracle
-on the host cores on a bounded sample of the same workload.
+average duration for the roofline figures, reported against the vendor peaks
+and against ceilings measured in the same run (a plain streaming read and a
+matrix-core loop).  The CPU baseline times the oracle on the host cores on a
+bounded sample of whole steps of the same workload (and on one thread for the
+two smallest workloads); its result also checks the timed step's decisions.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
@@ -185,6 +188,107 @@ def draft_host_timing(seconds=1.0):
             "what": "propose (trigger, retrieval, selection, tree) + commit (EMA, append), host, 1 thread"}
 
 
+def input_sha256(w):
+    """SHA-256 over every input array of the step (after the draft tokens are set)."""
+    import hashlib
+    import numpy as np
+    h = hashlib.sha256()
+    for k in ("hidden", "k_cache", "v_cache", "lm_head", "parent", "token", "src", "node_off", "kv_len"):
+        h.update(np.ascontiguousarray(getattr(w, k)).tobytes())
+    return h.hexdigest()
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def time_oracle_steps(oracle, w, seconds, min_steps=3, max_single=30.0):
+    """Whole oracle steps of w, timed one by one: at least min_steps (one if a step takes more
+    than max_single seconds) and until `seconds` have passed.  Returns (times, last result)."""
+    times, res = [], None
+    while len(times) < min_steps or sum(times) < seconds:
+        t1 = time.perf_counter()
+        res = oracle.verify_step(w)
+        times.append(time.perf_counter() - t1)
+        if times[0] > max_single:
+            break
+    return times, res
+
+
+def min_decision_margin(w, z):
+    """Smallest distance of a decision from its threshold in logits z: each row's top-1/top-2
+    gap, and each non-greedy draft token's distance from the tau and rank-k boundaries."""
+    import numpy as np
+    p = w.params
+    z32 = np.asarray(z, np.float32)
+    m = float("inf")
+    for b in range(len(w.node_off) - 1):
+        lo, hi = int(w.node_off[b]), int(w.node_off[b + 1])
+        for i in range(lo, hi):
+            t2 = np.partition(z32[i], -2)[-2:]
+            m = min(m, float(t2[1]) - float(t2[0]))
+        for j in range(lo + 1, hi):
+            row, t = z32[lo + int(w.parent[j])], int(w.token[j])
+            order = np.lexsort((np.arange(row.shape[0]), -row.astype(np.float64)))
+            if t == int(order[0]):
+                continue
+            m = min(m, abs(float(row[order[0]]) - float(row[t]) - p.tau))
+            r = int(np.nonzero(order == t)[0][0])
+            if p.topk < row.shape[0]:
+                m = min(m, float(row[t]) - float(row[order[p.topk]]) if r < p.topk
+                        else float(row[order[p.topk - 1]]) - float(row[t]))
+    return m
+
+
+def probe_ceilings(dev, stream):
+    """Measured ceilings: a plain 1 GiB streaming read (larger than the 256 MB MALL) and bf16
+    matrix-core loops of both MFMA shapes; the best of 5 launches of each configuration."""
+    import ctypes
+    import torch
+    from paper_2511_01282_amd import binding
+    L = binding.lib()
+    L.respec_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32,
+                                    ctypes.c_void_p, ctypes.c_void_p]
+    L.respec_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                    ctypes.c_void_p]
+    n = 1 << 30
+    buf = torch.empty(n, dtype=torch.uint8, device=dev)
+    sink = torch.empty(4096, dtype=torch.int32, device=dev)
+    wgs, iters = 4096, 1000
+    fsink = torch.empty(wgs * 256, dtype=torch.float32, device=dev)
+    s = stream.cuda_stream
+
+    def best(launch, count=5):
+        ts = []
+        for _ in range(count + 1):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            if launch() != 0:
+                raise RuntimeError("probe launch failed")
+            b.record(stream)
+            b.synchronize()
+            ts.append(a.elapsed_time(b) * 1e-3)
+        return min(ts[1:])
+
+    t_read = min(best(lambda: L.respec_probe_read(buf.data_ptr(), n, g, d, sink.data_ptr(), s))
+                 for g, d in ((1024, 8), (4096, 8), (4096, 16)))
+    tf = {}
+    for shape, flops_each in ((0, 16384), (1, 32768)):
+        t = best(lambda: L.respec_probe_mfma(wgs, iters, shape, fsink.data_ptr(), s))
+        tf[shape] = wgs * 4 * iters * 8 * flops_each / t / 1e12
+    return {"read_GBps": round(n / t_read / 1e9, 1), "mfma_bf16_TFLOPs": round(max(tf.values()), 1),
+            "mfma_bf16_16x16x32_TFLOPs": round(tf[0], 1), "mfma_bf16_32x32x16_TFLOPs": round(tf[1], 1),
+            "what": "1 GiB read once with 16-byte loads (best of 1024 or 4096 workgroups, 8 or 16 loads in "
+                    "flight per thread); 4096 workgroups x 4 waves of 8 independent bf16 MFMA chains per shape; "
+                    "best of 5 launches"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -192,8 +296,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=1, help="workload shape (default: 7B-shaped 26-node verify)")
     ap.add_argument("--rotate", type=int, default=0, help="input copies rotated per step (0: enough to exceed MALL)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the CPU oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=8.0, help="time budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-stochastic", action="store_true", help="skip the speculative-sampling pass")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -219,18 +324,47 @@ def main():
     M = int(w.node_off[-1])
     B = len(w.kv_len)
 
+    # ---- CPU baseline leg: the oracle on the host cores, whole steps of this workload ----
+    # (its logits do not depend on the draft tokens, so its first step also gives the argmax
+    # that the workload's argmax-prefix rule needs, and its decisions check the GPU's below)
+    cpu, expected, prefix_from = None, None, "gpu argmax (no oracle run)"
+    if not args.no_cpu_baseline:
+        import oracle
+        nproc = oracle.threads()
+        log(f"[bench] timing the CPU oracle on the host ({nproc} threads)")
+        times, res = time_oracle_steps(oracle, w, args.cpu_seconds)
+        z = res["logits"]
+        w.token = synth.apply_prefix_rule(w, np.argmax(z.astype(np.float32), axis=1).astype(np.int32))
+        prefix_from = "oracle argmax"
+        expected = oracle.decide(w, z)
+        margin = min_decision_margin(w, z)
+        one = {}
+        for c in (0, 1):
+            oracle.set_threads(1)
+            wc = w if c == cfg else synth.generate(c)
+            tc, _ = time_oracle_steps(oracle, wc, 0.0)
+            one[f"C{c}"] = {"ms_per_step": round(float(np.median(tc)) * 1e3, 1), "runs": len(tc)}
+            log(f"[bench] oracle on 1 thread, workload {c}: {one[f'C{c}']['ms_per_step']} ms/step")
+        oracle.set_threads(nproc)
+        med = float(np.median(times))
+        cpu = {"value": round(1.0 / med, 4), "unit": "steps/s", "cores": nproc, "kind": "oracle",
+               "sample": f"{len(times)} whole steps of the same workload (attention, LM head, vocab statistics, "
+                         f"acceptance, path), float64, {sum(times):.1f} s; value = 1 / median step time",
+               "ms_per_step_median": round(med * 1e3, 1), "ms_per_step_min": round(min(times) * 1e3, 1),
+               "cpu_model": cpu_model(), "one_thread": one}
+
     plan = runner.make_plan(w, dev)
     base = runner.upload(w, dev)
     kw = runner.step_kwargs(w)
     out = binding.alloc_outputs(total_nodes=M, batch=B, hidden=shp.hidden, vocab=shp.vocab,
                                 topk_out=shp.topk_out, max_depth=shp.max_depth, device=dev, attn_out=False)
-
-    # draft tokens: the workload's argmax-prefix rule, using the GPU's own argmax
-    plan.step(base, out, **kw)
-    torch.cuda.synchronize()
-    argmax = out["argmax"].cpu().numpy()
-    w.token = synth.apply_prefix_rule(w, argmax)
-    base["token"].copy_(torch.from_numpy(w.token.astype(np.int32)))
+    if expected is None:
+        # draft tokens: the workload's argmax-prefix rule, using the GPU's own argmax
+        plan.step(base, out, **kw)
+        torch.cuda.synchronize()
+        w.token = synth.apply_prefix_rule(w, out["argmax"].cpu().numpy())
+        base["token"].copy_(torch.from_numpy(w.token.astype(np.int32)))
+    sha = input_sha256(w)
 
     set_bytes = sum(base[k].numel() * base[k].element_size() for k in ("k_cache", "v_cache", "lm_head", "hidden"))
     R = args.rotate or max(2, math.ceil(4 * MALL_BYTES / set_bytes))
@@ -257,6 +391,18 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / K
+
+    # the timed steps' outputs (every set holds the same inputs) against the oracle's decisions
+    check = {"checked": False}
+    if expected is not None:
+        got = {k: out[k].cpu().numpy() for k in ("argmax", "flags", "path", "acc_len", "bonus", "winner_leaf",
+                                                 "leaf_acc_len", "seq_status")}
+        mism = {k: int((got[k] != expected[k]).sum()) for k in got}
+        check = {"checked": True, "agrees": not any(mism.values()), "mismatches": mism,
+                 "min_decision_margin": float(f"{margin:.3g}"), "acc_len": got["acc_len"].tolist(),
+                 "what": "argmax, flags, path, acc_len, bonus, winner, per-leaf lengths and statuses of the last "
+                         "timed step, bit for bit against the oracle (float64) on the same inputs"}
+        log(f"[bench] self-check against the oracle: {'agrees' if check['agrees'] else mism}")
 
     # per-stage durations: a second pass of K steps with HIP events that the library
     # takes from the kernels' own dispatches (start of attention, end of the split
@@ -291,57 +437,79 @@ def main():
         "step_us_p50": float(np.percentile(st["step"], 50)) * 1e3,
         "step_us_p90": float(np.percentile(st["step"], 90)) * 1e3,
     }
-    # stochastic verification (speculative sampling, Section 3.4 for drafter outputs) on the
-    # same inputs: drafter distributions near the target's (softmax of the logits plus
-    # N(0, 0.5^2) noise) and seeded uniforms, made before the timed region
-    g = torch.Generator(device=dev)
-    g.manual_seed(5)
-    q = torch.softmax(out["logits"] + 0.5 * torch.randn(out["logits"].shape, generator=g, device=dev), dim=-1)
-    q = q.contiguous()
-    u = torch.rand((M, 2), generator=g, device=dev)
-    out_s = binding.alloc_outputs(total_nodes=M, batch=B, hidden=shp.hidden, vocab=shp.vocab,
-                                  topk_out=shp.topk_out, max_depth=shp.max_depth, device=dev, attn_out=False)
-    sets_s = [dict(x, draft_prob=q, uniform=u) for x in sets]
-    kw_s = dict(kw, stochastic=1, temperature=1.0)
-    for i in range(max(2, args.warmup // 4)):
-        plan.step(sets_s[i % R], out_s, stream=stream, **kw_s)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(K):
-        plan.step(sets_s[i % R], out_s, stream=stream, **kw_s)
-    torch.cuda.synchronize()
-    wall_s = time.perf_counter() - t0
-    evs_s = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
-    for row in evs_s:
-        for e in row:
-            e.record(stream)
-    torch.cuda.synchronize()
-    for i in range(K):
-        plan.step(sets_s[i % R], out_s, stream=stream, stage_events=evs_s[i], **kw_s)
-    torch.cuda.synchronize()
-    stochastic = {
-        "steps_per_s": round(K / wall_s, 2), "us_per_step": round(wall_s * 1e6 / K, 2),
-        "vocab_pass_us": round(float(np.mean([r[2].elapsed_time(r[3]) for r in evs_s])) * 1e3, 3),
-        "mean_accepted": round(float(out_s["acc_len"].float().mean().item()), 3),
-        "what": "same step with speculative-sampling verification (temperature 1); the vocabulary "
-                "stage includes the sampling walk",
-    }
-    log(f"[bench] stochastic: {stochastic['us_per_step']:.1f} us/step, vocab stage {stochastic['vocab_pass_us']:.1f} us")
+    stochastic = None
+    if not args.no_stochastic:
+        # stochastic verification (speculative sampling, Section 3.4 for drafter outputs) on the
+        # same inputs: drafter distributions near the target's (softmax of the logits plus
+        # N(0, 0.5^2) noise) and seeded uniforms, made before the timed region
+        g = torch.Generator(device=dev)
+        g.manual_seed(5)
+        q = torch.softmax(out["logits"] + 0.5 * torch.randn(out["logits"].shape, generator=g, device=dev), dim=-1)
+        q = q.contiguous()
+        u = torch.rand((M, 2), generator=g, device=dev)
+        out_s = binding.alloc_outputs(total_nodes=M, batch=B, hidden=shp.hidden, vocab=shp.vocab,
+                                      topk_out=shp.topk_out, max_depth=shp.max_depth, device=dev, attn_out=False)
+        sets_s = [dict(x, draft_prob=q, uniform=u) for x in sets]
+        kw_s = dict(kw, stochastic=1, temperature=1.0)
+        for i in range(max(2, args.warmup // 4)):
+            plan.step(sets_s[i % R], out_s, stream=stream, **kw_s)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(K):
+            plan.step(sets_s[i % R], out_s, stream=stream, **kw_s)
+        torch.cuda.synchronize()
+        wall_s = time.perf_counter() - t0
+        evs_s = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+        for row in evs_s:
+            for e in row:
+                e.record(stream)
+        torch.cuda.synchronize()
+        for i in range(K):
+            plan.step(sets_s[i % R], out_s, stream=stream, stage_events=evs_s[i], **kw_s)
+        torch.cuda.synchronize()
+        stochastic = {
+            "steps_per_s": round(K / wall_s, 2), "us_per_step": round(wall_s * 1e6 / K, 2),
+            "vocab_pass_us": round(float(np.mean([r[2].elapsed_time(r[3]) for r in evs_s])) * 1e3, 3),
+            "mean_accepted": round(float(out_s["acc_len"].float().mean().item()), 3),
+            "what": "same step with speculative-sampling verification (temperature 1); the vocabulary "
+                    "stage includes the sampling walk",
+        }
+        log(f"[bench] stochastic: {stochastic['us_per_step']:.1f} us/step, vocab stage "
+            f"{stochastic['vocab_pass_us']:.1f} us")
+
+    ceil = probe_ceilings(dev, stream)
+    log(f"[bench] measured ceilings: read {ceil['read_GBps']} GB/s, bf16 MFMA {ceil['mfma_bf16_TFLOPs']} TFLOP/s "
+        f"(16x16x32: {ceil['mfma_bf16_16x16x32_TFLOPs']})")
 
     dom = max(("attention", "lm_head", "vocab_pass"), key=lambda k: stages[k]["us"])
     achieved = stages[dom]["GB/s"]
     traffic = lmhead_traffic(cfg) if dom == "lm_head" else None
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic}
+    # every stage against the vendor peaks and the measured ceilings, with the targets
+    # (>= 60 % of HBM for the attention and vocabulary passes, >= 50 % bf16 MFMA for the LM head)
+    peak_tf = BF16_PEAK_TFLOPS if shp.dtype == "bf16" else FP32_PEAK_TFLOPS
+    ai = nb["lm_flops"] / nb["lm"]
+    attainable = min(peak_tf, ai * HBM_PEAK_GBS / 1e3)
+    per_stage = {}
+    for k in ("attention", "vocab_pass", "lm_head"):
+        gbs = stages[k]["GB/s"]
+        per_stage[k] = {"GB/s": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+                        "frac_measured_read": round(gbs / ceil["read_GBps"], 4)}
+    per_stage["attention"]["target_frac_hbm"] = 0.6
+    per_stage["vocab_pass"]["target_frac_hbm"] = 0.6
+    tf = stages["lm_head"]["TFLOP/s"]
+    per_stage["lm_head"].update({
+        "TFLOP/s": round(tf, 1), "mfma_frac_peak": round(tf / peak_tf, 4),
+        "mfma_frac_measured": round(tf / ceil["mfma_bf16_TFLOPs"], 4) if shp.dtype == "bf16" else None,
+        "target_mfma_frac": 0.5, "arithmetic_intensity": round(ai, 1),
+        "attainable_tflops": round(attainable, 1), "frac_of_attainable": round(tf / attainable, 4)})
+    roofline["stages"] = per_stage
+    roofline["measured_ceilings"] = ceil
     if dom == "lm_head":
-        # the matrix-core view of the same kernel: its fraction of the dense peak, and of the
-        # attainable roofline min(peak, arithmetic intensity x HBM peak) at this token count
-        peak_tf = BF16_PEAK_TFLOPS if shp.dtype == "bf16" else FP32_PEAK_TFLOPS
-        ai = nb["lm_flops"] / nb["lm"]
-        attainable = min(peak_tf, ai * HBM_PEAK_GBS / 1e3)
-        roofline["mfma_frac"] = round(stages["lm_head"]["TFLOP/s"] / peak_tf, 4)
+        roofline["mfma_frac"] = per_stage["lm_head"]["mfma_frac_peak"]
         roofline["attainable_tflops"] = round(attainable, 1)
-        roofline["frac_of_attainable"] = round(stages["lm_head"]["TFLOP/s"] / attainable, 4)
+        roofline["frac_of_attainable"] = per_stage["lm_head"]["frac_of_attainable"]
     log(f"[bench] {ms_step * 1e3:.1f} us/step; stages " +
         ", ".join(f"{k} {stages[k]['us']:.1f} us" for k in ("attention", "lm_head", "vocab_pass")))
 
@@ -355,31 +523,19 @@ def main():
         torch.mul(a, 2.0, out=b)
         torch.cuda.synchronize()
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        import oracle
-        log("[bench] timing the CPU oracle on the host")
-        n_done, t_cpu = 0, 0.0
-        while t_cpu < args.cpu_seconds or n_done == 0:
-            t1 = time.perf_counter()
-            oracle.verify_step(w)
-            t_cpu += time.perf_counter() - t1
-            n_done += 1
-        cpu = {"value": round(n_done / t_cpu, 4), "unit": "steps/s", "cores": oracle.threads(), "kind": "oracle",
-               "sample": f"{n_done} full steps of the same workload (attention, LM head, vocab statistics, "
-                         f"acceptance, path), float64, {t_cpu:.1f} s"}
-
     draft_host = None if args.no_cpu_baseline else draft_host_timing()
 
     wl = {"workload": f"{shp.name}: {shp.dtype}, hidden {shp.hidden}, heads {shp.n_q_heads}/{shp.n_kv_heads}, "
                       f"head_dim {shp.head_dim}, vocab {shp.vocab}, batch {B}, nodes {M}, "
-                      f"KV len {int(w.kv_len.max())}", "config_index": cfg, "rotated_input_sets": R}
+                      f"KV len {int(w.kv_len.max())}", "config_index": cfg, "rotated_input_sets": R,
+          "input_sha256": sha, "draft_tokens": f"argmax-prefix rule from the {prefix_from}"}
     res = {
         "metric": "tree-verify steps/sec (attn+LM-head+accept), % of HBM and MFMA roofline",
         "value": round(K / wall, 2), "unit": "steps/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if shp.dtype == "bf16" else "f32", "data": "synthetic", "config": wl,
-        "roofline": roofline, "cpu_baseline": cpu, "draft_host": draft_host, "stochastic": stochastic,
+        "roofline": roofline, "cpu_baseline": cpu, "self_check": check, "draft_host": draft_host,
+        "stochastic": stochastic,
         "stages": {k: ({kk: round(vv, 3) for kk, vv in v.items()} if isinstance(v, dict) else round(v, 3))
                    for k, v in stages.items()},
         "device": torch.cuda.get_device_name(dev),

@@ -63,6 +63,7 @@ def _lib():
                                                 ctypes.c_float, _P, _P, _P]),
             "respec_oracle_lookahead": (_I32, [_I32, _P, _P, _I32, _I32]),
             "respec_oracle_threads": (_I32, []),
+            "respec_oracle_set_threads": (None, [_I32]),
             "respec_oracle_path": (None, [_I32, _P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P,
                                           _P, _P, _P]),
             "respec_oracle_stoch_node": (_I32, [_I32, _P, ctypes.c_float, _P, _I32, _P, _P, _P,
@@ -98,6 +99,11 @@ def _dt(w) -> int:
 def threads() -> int:
     """OpenMP threads used by the oracle's parallel loops."""
     return int(_lib().respec_oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """Set the OpenMP threads of the oracle's parallel loops (timing on 1 thread or on all)."""
+    _lib().respec_oracle_set_threads(int(n))
 
 
 def tree(parent, max_depth: int):

@@ -62,6 +62,9 @@
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int32_t respec_oracle_threads(void) { return (int32_t)omp_get_max_threads(); }
 
+/* Set that number (for timing the oracle on one thread and on all of them). */
+void respec_oracle_set_threads(int32_t n) { omp_set_num_threads(n > 0 ? n : 1); }
+
 static double bf16_to_double(uint16_t b) {
     uint32_t u = (uint32_t)b << 16;
     float f;

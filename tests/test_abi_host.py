@@ -37,6 +37,29 @@ def test_library_exports_every_declared_function(b):
         assert hasattr(b.lib(), name), name
 
 
+def test_library_exports_the_measurement_probes(b):
+    text = open(os.path.join(ROOT, "include", "respec_probe.h")).read()
+    names = sorted(set(re.findall(r"\b(respec_probe_[a-z_]+)\s*\(", text)))
+    assert names == ["respec_probe_mfma", "respec_probe_read"]
+    for name in names:
+        assert hasattr(b.lib(), name), name
+
+
+def test_probes_reject_bad_arguments_before_launch(b):
+    L = b.lib()
+    L.respec_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32,
+                                    ctypes.c_void_p, ctypes.c_void_p]
+    L.respec_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                    ctypes.c_void_p]
+    assert L.respec_probe_read(FAKE, 4096 * 8, 8, 3, FAKE, None) == 1          # depth
+    assert L.respec_probe_read(FAKE, 4096 * 8 + 16, 8, 8, FAKE, None) == 1     # not whole steps
+    assert L.respec_probe_read(FAKE + 8, 4096 * 8, 8, 8, FAKE, None) == 1      # alignment
+    assert L.respec_probe_read(None, 4096 * 8, 8, 8, FAKE, None) == 1
+    assert L.respec_probe_mfma(0, 10, 0, FAKE, None) == 1
+    assert L.respec_probe_mfma(8, 10, 2, FAKE, None) == 1
+    assert L.respec_probe_mfma(8, 10, 0, None, None) == 1
+
+
 def test_status_strings(b):
     for code in range(11):
         assert b.status_string(code)
