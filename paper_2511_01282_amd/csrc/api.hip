@@ -137,8 +137,9 @@ respec_status respec_verify_create(const respec_verify_shape* shape, respec_veri
     // per wave: one row-major, swizzled V tile (bf16) or one transposed, padded V tile (float32)
     const size_t vt_bytes = es == 2 ? (size_t)nwaves * kKvTile * s.head_dim * es
                                     : (size_t)nwaves * s.head_dim * (kKvTile + kVtPad) * es;
+    // wave merge: every wave's O lane-major (D/16 x NB blocks of 64 x 16 bytes) plus its m and l
     const size_t merge_bytes =
-        p->wk > 1 ? ((size_t)nwaves * rb * (s.head_dim + 2) + (size_t)p->wr * rb) * 4 : 0;
+        p->wk > 1 ? (size_t)nwaves * ((size_t)(s.head_dim / 16) * p->nb * 64 * 16 + (size_t)2 * p->nb * 64 * 4) : 0;
     p->attn_lds = vt_bytes > merge_bytes ? vt_bytes : merge_bytes;
     p->attn_wg_target = kTargetWaves / nwaves;
   }
@@ -287,12 +288,13 @@ respec_status step_impl(const respec_verify_plan* plan, const respec_verify_args
   at.wk = plan->wk;
   at.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.head_dim));
   dim3 agrid(at.nsplit, s.n_kv_heads * plan->n_rowblk, flat ? 1 : a.batch);
-  const hipError_t ae =
-      plan->attn_shared
-          ? launch_tree_attn_shared(s.head_dim, plan->nb, plan->attn_stages, plan->attn_kg, agrid, plan->attn_threads,
-                                    plan->attn_lds, at, st, ev ? ev[0] : nullptr)
-          : launch_tree_attn(s.dtype, s.head_dim, plan->nb, agrid, plan->attn_threads, plan->attn_lds, at, st,
-                             ev ? ev[0] : nullptr);
+  hipError_t ae;
+  if (plan->attn_shared)
+    ae = launch_tree_attn_shared(s.head_dim, plan->nb, plan->attn_stages, plan->attn_kg, agrid, plan->attn_threads,
+                                 plan->attn_lds, at, st, ev ? ev[0] : nullptr);
+  else
+    ae = launch_tree_attn(s.dtype, s.head_dim, plan->nb, agrid, plan->attn_threads, plan->attn_lds, at, st,
+                          ev ? ev[0] : nullptr);
   if (ae != hipSuccess) return RESPEC_ERR_HIP;
   const int merge_rows = 256 / (s.head_dim / 4);
   dim3 mgrid(cdiv(plan->rows_per_wg, merge_rows), a.batch * s.n_kv_heads * plan->n_rowblk);

@@ -481,6 +481,79 @@ __device__ __forceinline__ void ancestor_bits(const int (&qnode)[NB], int p_lo, 
   }
 }
 
+// The workgroup's unnormalised partial (O, reference max m, sum l) of each of its
+// rows, from the waves' accumulators (after the row-wide sum of l).  With one
+// wave per row group it is stored directly; otherwise the wk waves of a row group
+// combine their (O, m, l) through LDS (s_work, LDS no longer read by any wave).
+template <int D, int NB>
+__device__ __forceinline__ void store_partial(const AttnArgs& a, unsigned char* s_work, const f32x4 (&o)[D / 16][NB],
+                                              const float (&m_run)[NB], const float (&l_run)[NB], size_t pbase,
+                                              int wave, int nwaves, int lane) {
+  constexpr int DB = D / 16;
+  constexpr int RB = 16 * NB;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int wr = wave % a.wr, wk = wave / a.wr;
+  if (a.wk == 1) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int rl = wr * RB + 16 * nb + lr;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        *reinterpret_cast<f32x4*>(a.part_o + (pbase + rl) * D + 16 * db + 4 * lg) = o[db][nb];
+      if (lg == 0) {
+        a.part_m[pbase + rl] = m_run[nb];
+        a.part_l[pbase + rl] = l_run[nb];
+      }
+    }
+  } else {
+    // The wk waves of a row group combine their (O, m, l) through LDS.  Every wave
+    // stores its accumulators lane-major (so[wave][db][nb][lane], 16 bytes per lane:
+    // consecutive lanes write consecutive addresses, no bank conflicts), then each wave
+    // of the group combines the output blocks db = wk, wk + a.wk, ... of the group's
+    // rows in registers, lane by lane (every wave holds row lr + 16 nb, columns
+    // 16 db + 4 lg + i, in the same lane):
+    //   M = max_k m_k,  w_k = 2^(m_k - M),  l = sum_k w_k l_k,  O = sum_k w_k O_k.
+    __syncthreads();  // every wave is done with its V tiles
+    f32x4* so = reinterpret_cast<f32x4*>(s_work);                       // [nwaves][DB][NB][64]
+    float* sm = reinterpret_cast<float*>(so + (size_t)nwaves * DB * NB * 64);  // [nwaves][NB][64]
+    float* sl = sm + nwaves * NB * 64;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) so[((wave * DB + db) * NB + nb) * 64 + lane] = o[db][nb];
+      sm[(wave * NB + nb) * 64 + lane] = m_run[nb];
+      sl[(wave * NB + nb) * 64 + lane] = l_run[nb];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      float M = kNegInf;
+      for (int k = 0; k < a.wk; ++k) M = fmaxf(M, sm[((wr + a.wr * k) * NB + nb) * 64 + lane]);
+      float wgt[4], Ls = 0.f;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int wv = wr + a.wr * k;
+        const float mk = k < a.wk ? sm[(wv * NB + nb) * 64 + lane] : kNegInf;
+        wgt[k] = mk == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mk - M);
+        Ls += k < a.wk ? sl[(wv * NB + nb) * 64 + lane] * wgt[k] : 0.f;
+      }
+      const int rl = wr * RB + 16 * nb + lr;
+      for (int db = wk; db < DB; db += a.wk) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (k < a.wk) acc += so[(((wr + a.wr * k) * DB + db) * NB + nb) * 64 + lane] * wgt[k];
+        *reinterpret_cast<f32x4*>(a.part_o + (pbase + rl) * D + 16 * db + 4 * lg) = acc;
+      }
+      if (wk == 0 && lg == 0) {
+        a.part_m[pbase + rl] = M;
+        a.part_l[pbase + rl] = Ls;
+      }
+    }
+  }
+
+}
+
 // Rows of sequence b's KV range (prefix + tree); invalid device data degrades
 // to an empty sequence.  The merge computes the same, so both agree on the
 // flat partition.
@@ -683,63 +756,7 @@ __device__ __forceinline__ void attn_segment(const AttnArgs& a, unsigned char* s
   // ---- workgroup partial: (O unnormalised, max, sum) per row ----
   const int bgr = (b * a.n_kv_heads + g) * a.n_rowblk + rb;
   const size_t pbase = ((size_t)bgr * a.nsplit + split) * a.rows_per_wg;
-  if (a.wk == 1) {
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int rl = wr * RB + 16 * nb + lr;
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-        *reinterpret_cast<f32x4*>(a.part_o + (pbase + rl) * D + 16 * db + 4 * lg) = o[db][nb];
-      if (lg == 0) {
-        a.part_m[pbase + rl] = m_run[nb];
-        a.part_l[pbase + rl] = l_run[nb];
-      }
-    }
-  } else {
-    __syncthreads();  // every wave is done with its V tiles
-    float* mo = reinterpret_cast<float*>(s_work);  // [nwaves][RB][D]
-    float* mm = mo + (size_t)nwaves * RB * D;     // [nwaves][RB]   then weights
-    float* ml = mm + nwaves * RB;                 // [nwaves][RB]
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int rr = 16 * nb + lr;
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-        *reinterpret_cast<f32x4*>(mo + ((size_t)wave * RB + rr) * D + 16 * db + 4 * lg) = o[db][nb];
-      if (lg == 0) {
-        mm[wave * RB + rr] = m_run[nb];
-        ml[wave * RB + rr] = l_run[nb];
-      }
-    }
-    __syncthreads();
-    // per row: max over the wk waves of its row group, weights 2^(m_k - M), merged sum
-    for (int rl = threadIdx.x; rl < a.rows_per_wg; rl += blockDim.x) {
-      const int gr = rl / RB, rr = rl - gr * RB;
-      float M = kNegInf;
-      for (int k = 0; k < a.wk; ++k) M = fmaxf(M, mm[(gr + a.wr * k) * RB + rr]);
-      float Ls = 0.f;
-      for (int k = 0; k < a.wk; ++k) {
-        const int wv = gr + a.wr * k;
-        const float wgt = M == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mm[wv * RB + rr] - M);
-        Ls += ml[wv * RB + rr] * wgt;
-        mm[wv * RB + rr] = wgt;
-      }
-      a.part_m[pbase + rl] = M;
-      a.part_l[pbase + rl] = Ls;
-    }
-    __syncthreads();
-    constexpr int D4 = D / 4;
-    for (int idx = threadIdx.x; idx < a.rows_per_wg * D4; idx += blockDim.x) {
-      const int rl = idx / D4, d = (idx - rl * D4) * 4;
-      const int gr = rl / RB, rr = rl - gr * RB;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      for (int k = 0; k < a.wk; ++k) {
-        const int wv = gr + a.wr * k;
-        acc += *reinterpret_cast<const f32x4*>(mo + ((size_t)wv * RB + rr) * D + d) * mm[wv * RB + rr];
-      }
-      *reinterpret_cast<f32x4*>(a.part_o + (pbase + rl) * D + d) = acc;
-    }
-  }
+  store_partial<D, NB>(a, s_work, o, m_run, l_run, pbase, wave, nwaves, lane);
 }
 
 template <typename T, int D, int NB, bool Flat>
