@@ -69,35 +69,41 @@ def stage_bytes(w, M, es):
     return dict(attn=attn, lm=lm, vocab=vocab, attn_flops=attn_flops, lm_flops=lm_flops)
 
 
-def lmhead_source_hash():
-    """Hash of what the LM-head kernel is compiled from: lmhead.hip, common.hpp and the
-    LmArgs struct of kernels.hpp (the other launch declarations there do not change it)."""
+STAGE_SOURCES = {"attention": ("attention.hip", "AttnArgs"), "lm_head": ("lmhead.hip", "LmArgs"),
+                 "vocab_pass": ("vocab.hip", "VocabArgs")}
+
+
+def stage_source_hash(stage):
+    """Hash of what a stage's kernels are compiled from: its .hip file, common.hpp and its
+    argument struct in kernels.hpp (the other declarations there do not change it)."""
     import hashlib
+    src, struct = STAGE_SOURCES[stage]
     csrc = os.path.join(ROOT, "paper_2511_01282_amd", "csrc")
     h = hashlib.sha256()
-    for f in ("lmhead.hip", "common.hpp"):
+    for f in (src, "common.hpp"):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(fh.read())
     text = open(os.path.join(csrc, "kernels.hpp")).read()
-    a = text.index("struct LmArgs {")
+    a = text.index("struct %s {" % struct)
     h.update(text[a:text.index("};", a) + 2].encode())
     return h.hexdigest()[:16]
 
 
-def lmhead_traffic(cfg):
-    """HBM bytes per LM-head launch from the committed counter profile of the 7B-shaped
-    workload, or None when the kernel sources changed since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", "lmhead_7b_26node_hbm_traffic.txt")
-    if cfg != 1 or not os.path.exists(path):
+def stage_traffic(shape_name, stage):
+    """HBM bytes per launch of a stage's kernels from the committed counter profile of the
+    workload (FETCH_SIZE and WRITE_SIZE, calibrated), or None when there is none or the
+    stage's sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "verify_step_%s_hbm_traffic.txt" % shape_name.replace("-", "_"))
+    if not os.path.exists(path):
         return None
     fields = {}
     for line in open(path):
         parts = line.split()
-        if len(parts) >= 2 and parts[0] in ("lmhead_traffic_bytes", "lmhead_source_sha256_16"):
-            fields[parts[0]] = parts[1]
-    if fields.get("lmhead_source_sha256_16") != lmhead_source_hash():
+        if len(parts) == 3 and parts[0] in ("traffic_bytes", "source_sha256_16") and parts[1] == stage:
+            fields[parts[0]] = parts[2]
+    if "traffic_bytes" not in fields or fields.get("source_sha256_16") != stage_source_hash(stage):
         return None
-    return int(fields["lmhead_traffic_bytes"])
+    return int(fields["traffic_bytes"])
 
 
 def draft_host_timing(seconds=1.0):
@@ -483,7 +489,7 @@ def main():
 
     dom = max(("attention", "lm_head", "vocab_pass"), key=lambda k: stages[k]["us"])
     achieved = stages[dom]["GB/s"]
-    traffic = lmhead_traffic(cfg) if dom == "lm_head" else None
+    traffic = stage_traffic(shp.name, dom)
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic}
     # every stage against the vendor peaks and the measured ceilings, with the targets
@@ -495,7 +501,8 @@ def main():
     for k in ("attention", "vocab_pass", "lm_head"):
         gbs = stages[k]["GB/s"]
         per_stage[k] = {"GB/s": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
-                        "frac_measured_read": round(gbs / ceil["read_GBps"], 4)}
+                        "frac_measured_read": round(gbs / ceil["read_GBps"], 4),
+                        "bytes": int(stages[k]["bytes"]), "traffic": stage_traffic(shp.name, k)}
     per_stage["attention"]["target_frac_hbm"] = 0.6
     per_stage["vocab_pass"]["target_frac_hbm"] = 0.6
     tf = stages["lm_head"]["TFLOP/s"]
