@@ -571,6 +571,252 @@ __global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
   lmhead_tiled_body<TB, NVB>(a);
 }
 
+// ---------------------------------------------------------------------------
+// GEMM variant (bf16) for tiles of 256 token rows (129 or more rows in all).
+// A workgroup owns 128 vocabulary rows and MT = 256 token rows; every byte of
+// W and x it needs crosses its CU once:
+//   - K advances in 128-byte steps (64 elements); the W and x rows of a step go
+//     straight from memory into an LDS stage by DMA (global_load_lds, 16 bytes
+//     per lane, no registers), in a ring of S = 3 stages of 48 KB: after the
+//     barrier that publishes step c (every wave has finished step c-1 by then)
+//     step c+2 is requested into c-1's stage, so two steps are in flight while
+//     one is multiplied (the W and x rows of a step share a stage: giving W a
+//     deeper register ring of its own measured slower);
+//   - stage rows are 128 bytes with chunk c of row r stored at chunk position
+//     c ^ ((r >> 1) & 7): a quarter-wave reading one chunk of 16 consecutive
+//     rows touches all 64 banks once;
+//   - products on v_mfma_f32_32x32x16_bf16 with W as the A operand (32
+//     vocabulary rows) and x as the B operand (32 token rows); wave w owns
+//     vocabulary rows 64 (w & 1) .. +63 and token rows MT/2 (w >> 1) .. +MT/2-1;
+//     each step's fragments are requested ahead of its products;
+//   - a lane's accumulator holds, for token row (lane & 31) of a block, the
+//     vocabulary rows 8 g + 4 (lane >> 5) + e (g, e = 0..3) of a 32-row block;
+//   - the logits leave through LDS as a [token row][128] tile, so that each
+//     token row's 512 bytes are stored contiguously, and each thread reduces
+//     one token row of that tile to its two statistics tiles.
+constexpr int kGmVRows = 128;                   // vocabulary rows per workgroup
+constexpr int kGmTileRowB = kGmVRows * 4 + 16;  // LDS row stride of the logit tile (bytes)
+
+constexpr int kGmStep = 128;                    // bytes of a row per K step (64 elements)
+
+template <int MT>
+struct GmShape {
+  static constexpr int CPR = kGmStep / 16;                          // 16-byte chunks per stage row
+  static constexpr int RPI = 64 / CPR;                              // stage rows per DMA request
+  static constexpr int KS = kGmStep / 32;                           // 16-element slices per step
+  static constexpr int kStage = (MT + kGmVRows) * kGmStep;          // bytes per stage
+  static constexpr int S = 147456 / kStage;                         // stages (144 KB of LDS)
+  static constexpr int kXInst = MT / RPI / 4;                       // x DMA requests per wave per step
+  static constexpr int kWInst = kGmVRows / RPI / 4;                 // W DMA requests per wave per step
+  static constexpr int kPerStep = kXInst + kWInst;
+  static constexpr int NT = MT / 2 / 32;                            // 32-row token blocks per wave
+  static constexpr int kLds = S * kStage > MT * kGmTileRowB ? S * kStage : MT * kGmTileRowB;
+  static_assert(S >= 3 && (S - 1) * kPerStep <= 63, "stages and memory counter range");
+  // chunk position of chunk c of stage row r
+  static __device__ __forceinline__ int swz(int c, int r) { return c ^ ((r >> 1) & 7); }
+};
+
+// One 1 KB DMA request (8 rows of 128 bytes): lane l fills chunk position l % 8
+// of row 8 q + l / 8 with the chunk that belongs there.
+__device__ __forceinline__ void gm_dma(uint32_t lds_dst, uint64_t base, uint32_t off) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, %3\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_dst), "v"(off), "s"(base)
+      : "memory");
+}
+
+__device__ __forceinline__ uint64_t uniform_u64(uint64_t v) {
+  return ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32)) << 32) |
+         (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
+}
+
+template <int MT>
+__global__ __launch_bounds__(256) void lmhead_gemm_kernel(LmArgs a) {
+  using G = GmShape<MT>;
+  typedef float f32x16 __attribute__((ext_vector_type(16)));
+  __shared__ __align__(1024) unsigned char sm[G::kLds];
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)sm;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r32 = lane & 31, hi = lane >> 5;
+  const int n_mt = a.n_mtiles;
+  const int id = blockIdx.x;
+  const int grp = id / (8 * n_mt), rem = id % (8 * n_mt);
+  const int vt = grp * 8 + rem % 8, mt = rem / 8;  // the M tiles of a vocabulary tile share an XCD
+  if (vt * kGmVRows >= a.vocab) return;
+  const int v0 = vt * kGmVRows;
+  const int m0 = mt * MT;
+  const size_t row_bytes = (size_t)a.hidden_size * 2;
+  const int n_steps = (int)(row_bytes / kGmStep);  // >= 4 (hidden*2 is a multiple of 512; checked)
+  // K start: four phases, by vocabulary tile / 8 mod 4, so that the 32
+  // workgroups on one XCD (tiles congruent mod 8) stream x from four points
+  // (all from one point, or one each, measured slower)
+  const int rot = ((vt >> 3) & 3) * (n_steps / 4);
+
+  // this lane's DMA offsets (rows past M or V read a valid row; results not stored)
+  uint32_t xo[G::kXInst], wo[G::kWInst];
+#pragma unroll
+  for (int j = 0; j < G::kXInst; ++j) {
+    const int r = G::RPI * (wave * G::kXInst + j) + lane / G::CPR, pos = lane % G::CPR;
+    const int m = min(m0 + r, a.m_rows - 1);
+    xo[j] = (uint32_t)((size_t)(m - m0) * row_bytes + G::swz(pos, r) * 16);
+  }
+#pragma unroll
+  for (int j = 0; j < G::kWInst; ++j) {
+    const int r = G::RPI * (wave * G::kWInst + j) + lane / G::CPR, pos = lane % G::CPR;
+    const int v = min(v0 + r, a.vocab - 1);
+    wo[j] = (uint32_t)((size_t)(v - v0) * row_bytes + G::swz(pos, r) * 16);
+  }
+  const uint64_t xbase = reinterpret_cast<uint64_t>(a.x) + (uint64_t)m0 * row_bytes;
+  const uint64_t wbase = reinterpret_cast<uint64_t>(a.w) + (uint64_t)v0 * row_bytes;
+  auto issue = [&](int c) {  // requests of step c into stage c % S
+    const int kc = c + rot < n_steps ? c + rot : c + rot - n_steps;
+    const uint64_t ko = (uint64_t)kc * kGmStep;
+    const uint32_t st = lds0 + (uint32_t)((c % G::S) * G::kStage);
+    const uint64_t xb = uniform_u64(xbase + ko), wb = uniform_u64(wbase + ko);
+#pragma unroll
+    for (int j = 0; j < G::kXInst; ++j)
+      gm_dma(__builtin_amdgcn_readfirstlane(st + (uint32_t)((wave * G::kXInst + j) * 1024)), xb, xo[j]);
+#pragma unroll
+    for (int j = 0; j < G::kWInst; ++j)
+      gm_dma(__builtin_amdgcn_readfirstlane(st + (uint32_t)(MT * kGmStep + (wave * G::kWInst + j) * 1024)), wb,
+             wo[j]);
+  };
+
+  const int wv = wave & 1, wt = wave >> 1;
+  // LDS byte offsets of this lane's fragments within a 32-row block, per 16-element slice
+  uint32_t kof[G::KS];
+#pragma unroll
+  for (int ks = 0; ks < G::KS; ++ks) kof[ks] = (uint32_t)(r32 * kGmStep + G::swz(2 * ks + hi, r32) * 16);
+  const int a_row0 = MT + 64 * wv;     // stage row of the wave's first W row
+  const int b_row0 = wt * (MT / 2);    // stage row of the wave's first x row
+
+  f32x16 acc[2][G::NT];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int n = 0; n < G::NT; ++n) acc[i][n] = f32x16{};
+
+#pragma unroll
+  for (int j = 0; j < G::S - 1; ++j)
+    if (j < n_steps) issue(j);
+  for (int c = 0; c < n_steps; ++c) {
+    // step c's own requests have landed once at most the newer steps' are pending
+    if (c + G::S - 2 < n_steps)
+      asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"((G::S - 2) * G::kPerStep)
+                   : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if (c + G::S - 1 < n_steps) issue(c + G::S - 1);  // into the stage step c-1 used
+    const unsigned char* st = sm + (c % G::S) * G::kStage;
+    // (token blocks past the last row are multiplied too: clamped rows, not stored)
+    u32x4 af[G::KS][2], bfr[G::KS][G::NT];
+#pragma unroll
+    for (int ks = 0; ks < G::KS; ++ks) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        af[ks][i] = *reinterpret_cast<const u32x4*>(st + (a_row0 + 32 * i) * kGmStep + kof[ks]);
+#pragma unroll
+      for (int n = 0; n < G::NT; ++n)
+        bfr[ks][n] = *reinterpret_cast<const u32x4*>(st + (b_row0 + 32 * n) * kGmStep + kof[ks]);
+    }
+#pragma unroll
+    for (int ks = 0; ks < G::KS; ++ks)
+#pragma unroll
+      for (int n = 0; n < G::NT; ++n)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          acc[i][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[ks][i]),
+                                                              __builtin_bit_cast(bf16x8, bfr[ks][n]), acc[i][n], 0, 0, 0);
+    // schedule: the reads of slices 0 and 1, then each slice's products behind
+    // the reads of the slice after next
+    constexpr int kRd = 2 + G::NT, kMm = 2 * G::NT;
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * kRd, 0);
+#pragma unroll
+    for (int ks = 0; ks + 2 < G::KS; ++ks) {
+      __builtin_amdgcn_sched_group_barrier(0x008, kMm, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, kRd, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2 * kMm, 0);
+  }
+
+  // logits through LDS: the stages are free once every wave has finished the last step
+  __syncthreads();
+  unsigned char* tile = sm;  // [MT][kGmTileRowB] bytes
+#pragma unroll
+  for (int n = 0; n < G::NT; ++n)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int row = b_row0 + 32 * n + r32, col = 64 * wv + 32 * i + 8 * g + 4 * hi;
+        *reinterpret_cast<f32x4*>(tile + row * kGmTileRowB + col * 4) =
+            f32x4{acc[i][n][4 * g], acc[i][n][4 * g + 1], acc[i][n][4 * g + 2], acc[i][n][4 * g + 3]};
+      }
+  __syncthreads();
+  const int rows = min(MT, a.m_rows - m0);
+  {
+    const bool vec_ok = (a.vocab & 3) == 0;
+    const int col = 4 * r32;  // this lane's 4 vocabulary rows of a token row
+    const int vv = v0 + col;
+    for (int row = 2 * wave + hi; row < rows; row += 8) {  // two token rows per wave and pass
+      const f32x4 q = *reinterpret_cast<const f32x4*>(tile + row * kGmTileRowB + col * 4);
+      float* dst = a.logits + (size_t)(m0 + row) * a.vocab + vv;
+      if (vec_ok && vv + 3 < a.vocab) {
+        *reinterpret_cast<f32x4*>(dst) = q;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (vv + e < a.vocab) dst[e] = q[e];
+      }
+    }
+  }
+  if (!a.partials) return;
+
+  // statistics: thread t reduces token row t (and t + 256) over each 64-row statistics tile
+  for (int row = threadIdx.x; row < rows; row += 256) {
+#pragma unroll
+    for (int h = 0; h < kGmVRows / kLmTileRows; ++h) {
+      const int vh = v0 + kLmTileRows * h;
+      if (vh >= a.vocab) break;  // (no statistics tile past V)
+      const unsigned char* zr = tile + row * kGmTileRowB + h * kLmTileRows * 4;
+      float z[kLmTileRows];
+#pragma unroll
+      for (int q = 0; q < kLmTileRows / 4; ++q) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(zr + 16 * q);
+        z[4 * q] = v[0];
+        z[4 * q + 1] = v[1];
+        z[4 * q + 2] = v[2];
+        z[4 * q + 3] = v[3];
+      }
+      const int nv = a.vocab - vh;  // entries at or past V are not logits
+      float mx = kNegInf;
+#pragma unroll
+      for (int i = 0; i < kLmTileRows; ++i) mx = i < nv ? fmaxf(mx, z[i]) : mx;
+      float S = 0.f, T = 0.f;
+      int am = 0x7FFFFFFF;
+#pragma unroll
+      for (int i = kLmTileRows - 1; i >= 0; --i) {
+        const bool ok = i < nv;
+        const float d = z[i] - mx;
+        const float e = ok ? __expf(d) : 0.f;
+        S += e;
+        T += ok ? e * d : 0.f;
+        am = (ok && z[i] == mx) ? vh + i : am;
+      }
+      *reinterpret_cast<u32x4*>(a.partials + ((size_t)(m0 + row) * a.n_vtiles + vh / kLmTileRows) * kTileWords) =
+          u32x4{__float_as_uint(mx), __float_as_uint(S), __float_as_uint(T), (uint32_t)am};
+    }
+  }
+}
+
 // Workgroups of a kernel that fit on the device at once (host occupancy
 // query, cached per kernel; 0 if the query fails).
 template <typename F>
@@ -616,13 +862,17 @@ hipError_t launch_lmhead(int dtype, int mb, bool wide, const LmArgs& a, hipStrea
   const int n_vt = (a.vocab + kLmRows - 1) / kLmRows;
   const int n_grp = (n_vt + 7) / 8;
   dim3 grid(n_grp * 8 * a.n_mtiles);
-  if (mb == 8 || mb == 16) {  // tiled variant: MT = 128 or 256 token rows, 128-row vocabulary tiles (bf16)
+  if (mb == 8) {  // tiled variant: 65-128 token rows, 128-row vocabulary tiles (bf16)
     if (dtype != 1) return hipErrorInvalidValue;
     const int n_vt2 = (a.vocab + 127) / 128;
     dim3 tgrid(((n_vt2 + 7) / 8) * 8 * a.n_mtiles);
-    const dim3 blk(256);
-    return mb == 8 ? launch_k(lmhead_tiled_kernel<2, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a)
-                   : launch_k(lmhead_tiled_kernel<4, 8>, tgrid, blk, 0, s, nullptr, ev_stop, a);
+    return launch_k(lmhead_tiled_kernel<2, 8>, tgrid, dim3(256), 0, s, nullptr, ev_stop, a);
+  }
+  if (mb == 16) {  // GEMM variant: 256 token rows per tile, 128-row vocabulary tiles (bf16)
+    if (dtype != 1 || a.hidden_size % 256 != 0) return hipErrorInvalidValue;
+    const int n_vt2 = (a.vocab + kGmVRows - 1) / kGmVRows;
+    dim3 tgrid(((n_vt2 + 7) / 8) * 8 * a.n_mtiles);
+    return launch_k(lmhead_gemm_kernel<256>, tgrid, dim3(256), 0, s, nullptr, ev_stop, a);
   }
   if (wide) {  // wide tiled variant: up to 64 token rows, 256-row vocabulary tiles (bf16)
     if (dtype != 1 || mb > 4) return hipErrorInvalidValue;

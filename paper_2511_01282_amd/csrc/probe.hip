@@ -33,9 +33,13 @@ __global__ __launch_bounds__(256) void probe_read_kernel(const char* buf, size_t
   if (threadIdx.x == 0) sink[blockIdx.x] = sh[0] ^ sh[1] ^ sh[2] ^ sh[3];
 }
 
+// Eight independent accumulation chains per wave, issued back to back.  The
+// instructions are inline assembly with the accumulators updated in place:
+// written as builtins, the compiler rotates the chains through other registers
+// every iteration (several VALU copies per product), which measures the copies.
 template <int SHAPE>
 __global__ __launch_bounds__(256) void probe_mfma_kernel(int iters, float* sink) {
-  // operands from the thread index (not known at compile time); 8 independent chains
+  // operands from the thread index (not known at compile time)
   typedef float f32x16 __attribute__((ext_vector_type(16)));
   const uint32_t t = threadIdx.x + 1;
   const u32x4 a = {t * 0x3F800000u & 0x3F803F80u, 0x3F803F80u, t & 0x00FF00FFu, 0x3C003C00u};
@@ -47,7 +51,7 @@ __global__ __launch_bounds__(256) void probe_mfma_kernel(int iters, float* sink)
     for (int k = 0; k < 8; ++k) c[k] = f32x4{(float)k, 0.f, 0.f, 0.f};  // distinct chains
     for (int it = 0; it < iters; ++it) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) c[k] = mma_k64(bf16_t{}, a, b, c[k]);
+      for (int k = 0; k < 8; ++k) asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c[k]) : "v"(a), "v"(b));
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k) total += c[k].x + c[k].y + c[k].z + c[k].w;
@@ -60,9 +64,7 @@ __global__ __launch_bounds__(256) void probe_mfma_kernel(int iters, float* sink)
     }
     for (int it = 0; it < iters; ++it) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
-        c[k] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
-                                                       c[k], 0, 0, 0);
+      for (int k = 0; k < 8; ++k) asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(c[k]) : "v"(a), "v"(b));
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k)
