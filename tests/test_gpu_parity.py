@@ -258,6 +258,32 @@ def test_vocab_tier_parity(rt, vocab, topk_out, mode):
     compare(case, rt.run(case.w, tok_rank=True), f"vocab {vocab}")
 
 
+# The LM head's GEMM form (bf16, more than 128 token rows in all): 256-row token
+# tiles with rows past M, a vocabulary that is not a multiple of 4 (the logit
+# rows are unaligned: scalar stores) nor of the 128-row vocabulary tile, and
+# (300 nodes) a second token tile.
+GEMM_CASES = {
+    "218-nodes": [[-1] + [(j - 1) // 3 for j in range(1, 128)], [-1] + [(j - 1) // 2 for j in range(1, 90)]],
+    "300-nodes": [[-1] + [(j - 1) // 3 for j in range(1, 128)], [-1] + [(j - 1) // 2 for j in range(1, 100)],
+                  [-1] + [j - 1 for j in range(1, 60)], [-1] + [0] * 12],
+}
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("name", list(GEMM_CASES))
+def test_gemm_lm_head_parity(rt, name):
+    parents = GEMM_CASES[name]
+    depth = max(8, max(_depth(p) for p in parents))
+    shp = synth.Shape("edge", "bf16", 4 * 64, 4, 2, 64, 3001, len(parents), max(len(p) for p in parents), depth, 8)
+    # (the cache capacity covers the longest prefix plus the largest tree: the 128-node tree has the longest)
+    w = synth.custom(shp, parents, [300, 90, 150, 20][:len(parents)], seed=505, poison_tail=True)
+    assert int(w.node_off[-1]) > 128
+    _say(f"[gemm {name}] building")
+    case = workload.finish(w)
+    _say(f"[gemm {name}] running GPU step")
+    compare(case, rt.run(case.w, x_out=True, tok_rank=True), f"gemm {name}")
+
+
 def _depth(parent):
     d = [0] * len(parent)
     for j in range(1, len(parent)):
