@@ -534,6 +534,12 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
   const float* zrow = a.logits + (size_t)i * a.vocab;
   uint64_t* sv = sh.surv[wave];
   int nv = 0;
+  // More candidate tiles than the list holds only happens when tile keys repeat,
+  // which statistics written by the LM head never do (a tile's argmax lies in
+  // that tile); the wave then reads all of its own tiles instead, and never
+  // indexes past the list.
+  const bool cand_over = nt > kMaxCandTiles;  // (uniform over the wave)
+  nt = min(nt, kMaxCandTiles);
   auto cand_pass = [&](int p0, uint64_t (&kz)[8]) {
     const int c = p0 + (lane >> 3);
     const int col0 = c < nt ? ct[c] * kLmTileRows + (lane & 7) : a.vocab;
@@ -546,7 +552,7 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
       kz[e] = kv != 0 && kv >= H ? kv : 0ull;
     }
   };
-  if (!spill) {
+  if (!spill && !cand_over) {
     for (int p0 = 0; p0 < nt; p0 += 8) {
       uint64_t kz[8];
       cand_pass(p0, kz);
@@ -581,18 +587,28 @@ __device__ __forceinline__ void finalize_row(const VocabArgs& a, FinalizeLds<KO>
   // survivors, sorted across the wave; otherwise (many equal values, or rows
   // read whole) per-lane top-K lists and K rounds of wave maxima.
   uint64_t kk;
-  if (!spill && nv <= 64) {
+  if (!spill && !cand_over && nv <= 64) {
     kk = wave_sort_desc(lane < nv ? sv[lane] : 0ull);
   } else {
     uint64_t ck[KO];
 #pragma unroll
     for (int k = 0; k < KO; ++k) ck[k] = 0ull;
-    if (!spill) {
+    if (!spill && !cand_over) {
       for (int p0 = 0; p0 < nt; p0 += 8) {
         uint64_t kz[8];
         cand_pass(p0, kz);
 #pragma unroll
         for (int e = 0; e < 8; ++e) insert_desc<KO>(ck, kz[e]);
+      }
+    } else if (!spill) {  // every column of this thread's own tiles
+#pragma unroll
+      for (int u = 0; u < LB; ++u) {
+        const int t = tid + u * NT;
+        if (t >= a.n_vtiles) continue;
+        for (int e = 0; e < kLmTileRows; ++e) {
+          const int col = t * kLmTileRows + e;
+          if (col < a.vocab) insert_desc<KO>(ck, make_key(zrow[col], col));
+        }
       }
     } else {
       for (int col = tid; col < a.vocab; col += NT) insert_desc<KO>(ck, make_key(zrow[col], col));
