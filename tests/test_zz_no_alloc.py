@@ -84,6 +84,27 @@ def test_noalloc_smaller_batch_after_larger(rt):
         np.testing.assert_array_equal(got["acc_len"], case.expected["acc_len"], err_msg=label)
 
 
+@pytest.mark.timeout(600)
+def test_noalloc_gemm_lm_head_and_shared_tile_attention(rt):
+    # 218 token rows in two trees (the LM head's GEMM form), then a grouped-query
+    # batch on the shared-tile attention (8 query heads per KV head), then the
+    # first again: three plans in a row over one scratch
+    shp = synth.Shape("edge", "bf16", 4 * 64, 4, 2, 64, 3001, 2, 128, 8, 8)
+    parents = [[-1] + [(j - 1) // 3 for j in range(1, 128)], [-1] + [(j - 1) // 2 for j in range(1, 90)]]
+    gemm = workload.finish(synth.custom(shp, parents, [300, 90], seed=505, poison_tail=True))
+    shp2 = synth.Shape("edge", "bf16", 16 * 128, 16, 2, 128, 4000, 2, 40, 12, 8)
+    parents2 = [[-1] + [max(0, j - 4) for j in range(1, 40)], [-1, 0, 1, 1]]
+    gqa = workload.finish(synth.custom(shp2, parents2, [700, 60], seed=506, poison_tail=True))
+    for label, case in (("218 rows", gemm), ("grouped-query", gqa), ("218 rows again", gemm)):
+        print(f"[noalloc] {label}", flush=True)
+        ref = _run(rt, case, noalloc=False)
+        got = _run(rt, case, noalloc=True)
+        _same(got, ref, label)
+        e = case.expected
+        for k in ("argmax", "flags", "path", "acc_len", "bonus", "winner_leaf", "seq_status"):
+            np.testing.assert_array_equal(got[k], e[k], err_msg=f"{label}: {k} against the oracle")
+
+
 def test_noalloc_refuses_a_plan_beyond_the_scratch(rt):
     import torch
     from paper_2511_01282_amd import binding
