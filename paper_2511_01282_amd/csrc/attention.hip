@@ -38,6 +38,34 @@ __device__ __forceinline__ bool anc_has(const u32x4& w, int ai) {
   return (word >> (ai & 31)) & 1u;
 }
 
+// Maxima as single instructions.  Scores come straight from the matrix cores,
+// and fmaxf would first canonicalise each of them (one more instruction per
+// score); no score is a signalling NaN, so the plain instruction gives the
+// same maximum.
+__device__ __forceinline__ float max3_f32(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+__device__ __forceinline__ float max_f32(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+// Maximum of the 8 scores a lane holds for one query row (two 16-key halves of
+// a tile) and of the row's other three lane groups (lanes l ^ 16, l ^ 32,
+// l ^ 48).  A swap of odd and even 16-lane rows between two copies of x leaves
+// each lane's own and partner's values split over the two results, so their
+// maximum is the pair's maximum in every lane; the 32-lane swap does the same
+// for the halves.
+__device__ __forceinline__ float row_max8(f32x4 a, f32x4 b) {
+  float x = max_f32(max3_f32(a[0], a[1], a[2]), max3_f32(a[3], b[0], max3_f32(b[1], b[2], b[3])));
+  const auto h = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = max_f32(__uint_as_float(h[0]), __uint_as_float(h[1]));
+  const auto w = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return max_f32(__uint_as_float(w[0]), __uint_as_float(w[1]));
+}
+
 template <typename T, int D>
 struct AttnTile {
   static constexpr int ES = Elem<T>::kBytes;
@@ -144,11 +172,7 @@ __device__ __forceinline__ void process_tile(const AttnTile<T, D>& t, int t0, in
   // online softmax (row max shared by the 4 lane groups of a row)
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    float tm = kNegInf;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) tm = fmaxf(tm, fmaxf(fmaxf(s[kb][nb][0], s[kb][nb][1]), fmaxf(s[kb][nb][2], s[kb][nb][3])));
-    tm = fmaxf(tm, xchg<4>(tm));
-    tm = fmaxf(tm, xchg<5>(tm));
+    const float tm = row_max8(s[0][nb], s[1][nb]);
     // m_run is a reference maximum: it is raised only when a score exceeds it by more
     // than kLazyMargin (so p <= 2^kLazyMargin), and the accumulators are rescaled only
     // then; while it is unset (-inf) the accumulators are zero and need no rescale.
@@ -363,12 +387,7 @@ __device__ __forceinline__ void softmax_p_bf16(f32x4 (&s)[2][NB], int t0, int kv
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     if (nb >= nbc) break;  // row blocks past nbc hold no live row (wave-uniform)
-    float tm = kNegInf;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-      tm = fmaxf(tm, fmaxf(fmaxf(s[kb][nb][0], s[kb][nb][1]), fmaxf(s[kb][nb][2], s[kb][nb][3])));
-    tm = fmaxf(tm, xchg<4>(tm));
-    tm = fmaxf(tm, xchg<5>(tm));
+    const float tm = row_max8(s[0][nb], s[1][nb]);
     // m_run is a reference maximum: it is raised only when a score exceeds it by more
     // than kLazyMargin (so p <= 2^kLazyMargin), and the accumulators are rescaled only
     // then; while it is unset (-inf) the accumulators are zero and need no rescale.
@@ -825,22 +844,41 @@ __device__ __forceinline__ int kswz(int r) {
 // them.  The tile base is uniform (scalar registers), each lane adds a 32-bit
 // offset; M0 holds the LDS destination (saved and restored around the
 // request) and needs one wait state before the request.
+// Per-lane source offsets of a half-tile, one per DMA instruction (rows past
+// kv_hi clamped when the tile is not whole).  A whole tile's offsets do not
+// depend on the tile, so a requesting wave computes them once (DmaOffsets).
 template <int D, bool V>
-__device__ __forceinline__ void dma_half_asm(uint32_t lds_dst, const char* base, int t0, int kv_hi, int lane) {
-  constexpr int CPR = D * 2 / 16;  // 16-byte chunks per row
-  constexpr int RPI = 64 / CPR;    // rows per DMA instruction (1 KB)
+struct DmaLayout {
+  static constexpr int CPR = D * 2 / 16;  // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;    // rows per DMA instruction (1 KB)
+  static constexpr int N = kKvTile / RPI;
+  __device__ __forceinline__ static uint32_t at(int q, int lane, int t0, int kv_hi, bool full) {
+    const int r = q * RPI + lane / CPR, pos = lane % CPR;
+    const int c = pos ^ (V ? vswz<D>(r) : kswz<D>(r));  // chunk that belongs at position pos
+    const int rr = full ? r : min(t0 + r, kv_hi - 1) - t0;  // rows past kv_hi: row kv_hi - 1 (t0 <= kv_hi - 1)
+    return (uint32_t)(rr * D * 2 + c * 16);
+  }
+};
+template <int D>
+struct DmaOffsets {
+  uint32_t off[DmaLayout<D, false>::N];
+  __device__ __forceinline__ void init(bool v_half, int lane) {  // v_half uniform
+#pragma unroll
+    for (int q = 0; q < DmaLayout<D, false>::N; ++q)
+      off[q] = v_half ? DmaLayout<D, true>::at(q, lane, 0, kKvTile, true) : DmaLayout<D, false>::at(q, lane, 0, kKvTile, true);
+  }
+};
+
+template <int D, bool V>
+__device__ __forceinline__ void dma_half_asm(uint32_t lds_dst, const char* base, int t0, int kv_hi, int lane,
+                                             const DmaOffsets<D>& pre) {
+  using O = DmaLayout<D, V>;
   // the tile base and the LDS destination are uniform: made scalar explicitly for the asm operands
   const uint64_t tb_u = reinterpret_cast<uint64_t>(base + (size_t)t0 * D * 2);
   const uint64_t tb = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(tb_u >> 32)) << 32) |
                       (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)tb_u);
   lds_dst = __builtin_amdgcn_readfirstlane(lds_dst);
-  const bool full = t0 + kKvTile <= kv_hi;  // uniform
-#pragma unroll
-  for (int q = 0; q < kKvTile / RPI; ++q) {
-    const int r = q * RPI + lane / CPR, pos = lane % CPR;
-    const int c = pos ^ (V ? vswz<D>(r) : kswz<D>(r));  // chunk that belongs at position pos
-    const int rr = full ? r : min(t0 + r, kv_hi - 1) - t0;  // rows past kv_hi: row kv_hi - 1 (t0 <= kv_hi - 1)
-    const uint32_t off = (uint32_t)(rr * D * 2 + c * 16);
+  auto request = [&](int q, uint32_t off) {
     uint32_t saved;
     asm volatile(
         "s_mov_b32 %0, m0\n\t"
@@ -851,6 +889,13 @@ __device__ __forceinline__ void dma_half_asm(uint32_t lds_dst, const char* base,
         : "=&s"(saved)
         : "s"(lds_dst + q * 1024), "v"(off), "s"(tb)
         : "memory");
+  };
+  if (t0 + kKvTile <= kv_hi) {  // (uniform) a whole tile: the precomputed offsets
+#pragma unroll
+    for (int q = 0; q < O::N; ++q) request(q, pre.off[q]);
+  } else {
+#pragma unroll
+    for (int q = 0; q < O::N; ++q) request(q, O::at(q, lane, t0, kv_hi, false));
   }
 }
 
@@ -945,13 +990,15 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
 #pragma unroll
     for (int kc = 0; kc < KCH; ++kc) asm volatile("" : "+v"(qf[nb][kc]));
   // the first S - KG tiles (kv_hi >= 1, so every clamped row is a valid cache row)
+  DmaOffsets<D> doff;  // wave 0: K halves, wave 1: V halves
+  if (wave < 2) doff.init(wave == 1, lane);
   if (wave < 2) {
 #pragma unroll
     for (int st = 0; st < S - KG; ++st) {
       if (wave == 0)
-        dma_half_asm<D, false>(lds0 + st * kStage, kbase, tile_row(st), kv_hi, lane);
+        dma_half_asm<D, false>(lds0 + st * kStage, kbase, tile_row(st), kv_hi, lane, doff);
       else
-        dma_half_asm<D, true>(lds0 + st * kStage + kTile, vbase, tile_row(st), kv_hi, lane);
+        dma_half_asm<D, true>(lds0 + st * kStage + kTile, vbase, tile_row(st), kv_hi, lane, doff);
     }
   }
 
@@ -991,9 +1038,9 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
         sl = sl < 0 ? sl + S : sl;
         const int t_new = KG * j - KG + q + S;
         if (wave == 0)
-          dma_half_asm<D, false>(lds0 + sl * kStage, kbase, tile_row(t_new), kv_hi, lane);
+          dma_half_asm<D, false>(lds0 + sl * kStage, kbase, tile_row(t_new), kv_hi, lane, doff);
         else
-          dma_half_asm<D, true>(lds0 + sl * kStage + kTile, vbase, tile_row(t_new), kv_hi, lane);
+          dma_half_asm<D, true>(lds0 + sl * kStage + kTile, vbase, tile_row(t_new), kv_hi, lane, doff);
       }
     }
     const int t = KG * j + grp;
