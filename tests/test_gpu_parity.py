@@ -186,6 +186,10 @@ EDGE = {
     "d64-bf16-mixed": ("bf16", 4, 4, 64, [[-1, 0, 1, 2, 0, 4, 5, 1, 7]], [64]),
     # 96 query rows per KV head (three waves sharing each KV tile), head_dim 64
     "d64-bf16-shared-rows": ("bf16", 4, 2, 64, [[-1] + [j // 2 for j in range(0, 47)]], [300]),
+    # 136 query rows per KV head: one key group of five row waves, the last with one live
+    # row block of two (head_dim 64 and 128; the split ends fall inside KV tiles)
+    "d64-bf16-136-rows": ("bf16", 16, 2, 64, [[-1] + [max(0, j - 3) for j in range(1, 17)]], [500]),
+    "d128-bf16-136-rows": ("bf16", 8, 1, 128, [[-1] + [j // 2 for j in range(0, 16)]], [777]),
     "max-nodes-128": ("bf16", 2, 2, 128, [[-1] + [max(0, j - 4) for j in range(1, 128)]], [31]),
     "max-depth-64": ("bf16", 2, 2, 128, [[-1] + list(range(0, 64))], [5]),
     # LM-head tiles of 48 and 64 token rows (33-48 and 49-64 nodes) in float32 and bf16
