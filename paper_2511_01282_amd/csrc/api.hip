@@ -112,17 +112,17 @@ respec_status respec_verify_create(const respec_verify_shape* shape, respec_veri
   p->nb = nb;
   p->attn_shared = es == 2 && rg >= 2;
   if (p->attn_shared) {
-    // up to 8 waves of rows read every KV tile once, from a shared 8-slot LDS
-    // ring, one workgroup per CU; up to 4 waves of rows, a second key group of
-    // as many waves takes every other tile (one workgroup fills the CU, and
-    // its two halves stay in step)
+    // up to 8 waves of rows read every KV tile once, from a shared LDS ring,
+    // one workgroup per CU; up to 4 waves of rows, a second key group of as
+    // many waves takes every other tile (one workgroup fills the CU, and its
+    // two halves stay in step)
     p->wr = rg < 8 ? rg : 8;
     p->n_rowblk = cdiv(rg, p->wr);
     p->wk = 1;
     p->attn_kg = p->wr <= 4 ? 2 : 1;
     p->rows_per_wg = p->wr * rb;
     p->attn_threads = 64 * p->wr * p->attn_kg;
-    p->attn_stages = 8;
+    p->attn_stages = p->attn_kg == 1 ? kSharedStages1 : kSharedStages2;
     p->attn_lds = (size_t)shared_ring_bytes(s.head_dim, p->attn_stages);
     p->attn_wg_target = kCUs;
   } else {

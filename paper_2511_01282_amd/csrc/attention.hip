@@ -816,12 +816,14 @@ __global__ __launch_bounds__(256) void tree_attn_kernel(AttnArgs a) {
 // once per workgroup, straight into LDS by DMA (global_load_lds, 16 bytes per
 // lane), into a ring of S slots:
 //   - wave 0 requests the K half and wave 1 the V half of every tile;
-//   - tile i is consumed while tiles i+1 .. i+S-1 are in flight: a requesting
-//     wave waits until only its S-2 newest tiles are pending, then one barrier
-//     publishes tile i to every wave and, as every wave has finished tile i-1
-//     by then, frees that slot for tile i+S-1, requested right after (S = 5
-//     with two workgroups per CU, S = 8 with one); with S-1 tiles in flight
-//     the loop waits on its own arithmetic, not on HBM;
+//   - a pass consumes TP = KG*TPG tiles (each of the KG key groups takes TPG
+//     of them, in tile order) while the next S-TP are in flight: a requesting
+//     wave waits until only its S-2*TP newest tiles are pending, then one
+//     barrier publishes the pass's tiles to every wave and, as every wave has
+//     finished the previous pass by then, frees that pass's slots for the
+//     tiles S ahead, requested right after.  Several tiles per pass (one
+//     barrier for all of them) let the waves of a SIMD drift apart within the
+//     pass instead of meeting at every tile;
 //   - the DMA requests are inline assembly (see dma_half_asm), so the K
 //     fragments (A operand of S^T = K Q^T) and the transposed V fragments are
 //     ordinary LDS reads that the compiler schedules; the barrier's own waits
@@ -899,7 +901,7 @@ __device__ __forceinline__ void dma_half_asm(uint32_t lds_dst, const char* base,
   }
 }
 
-template <int D, int NB, int S, int KG>
+template <int D, int NB, int S, int KG, int TPG>
 __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
   constexpr int KCH = D * 2 / 64;
   constexpr int DB = D / 16;
@@ -907,7 +909,8 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
   constexpr int kTile = kKvTile * D * 2;  // bytes of one K or V half-tile
   constexpr int kStage = 2 * kTile;
   constexpr int kLpt = kTile / 1024;      // DMA instructions per half-tile
-  static_assert(S >= 2 * KG + 1 && (S - 2 * KG) * kLpt <= 63, "vmcnt holds at most 63 pending requests");
+  constexpr int TP = KG * TPG;            // tiles per pass
+  static_assert(S > 2 * TP && (S - 2 * TP) * kLpt <= 63, "vmcnt holds at most 63 pending requests");
 
   extern __shared__ __align__(16) unsigned char smem[];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)smem;
@@ -989,12 +992,12 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
   for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
     for (int kc = 0; kc < KCH; ++kc) asm volatile("" : "+v"(qf[nb][kc]));
-  // the first S - KG tiles (kv_hi >= 1, so every clamped row is a valid cache row)
+  // the first S - TP tiles (kv_hi >= 1, so every clamped row is a valid cache row)
   DmaOffsets<D> doff;  // wave 0: K halves, wave 1: V halves
   if (wave < 2) doff.init(wave == 1, lane);
   if (wave < 2) {
 #pragma unroll
-    for (int st = 0; st < S - KG; ++st) {
+    for (int st = 0; st < S - TP; ++st) {
       if (wave == 0)
         dma_half_asm<D, false>(lds0 + st * kStage, kbase, tile_row(st), kv_hi, lane, doff);
       else
@@ -1019,33 +1022,35 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
   // row blocks of this wave that hold a live row (blocks past the group's last row are skipped)
   const int nbc = __builtin_amdgcn_readfirstlane(min(NB, max(0, (R - row_wave + 15) / 16)));
 
-  // Pass j consumes tiles KG*j .. KG*j+KG-1 (group q takes tile KG*j+q) from
-  // slots s0 .. s0+KG-1 (mod S); the slots of the previous pass's tiles are
-  // refilled with the tiles S ahead of them.
-  int s0 = 0;  // ring slot of tile KG*j
-  for (int j = 0; KG * j < n_tiles; ++j) {
-    // tiles KG*j .. KG*j+KG-1 have landed (a requesting wave waits for its own
+  // Pass j consumes tiles TP*j .. TP*j+TP-1 (group q takes tiles TP*j + KG*r + q,
+  // r < TPG) from slots s0 .. s0+TP-1 (mod S); the slots of the previous pass's
+  // tiles are refilled with the tiles S ahead of them.
+  int s0 = 0;  // ring slot of tile TP*j
+  for (int j = 0; TP * j < n_tiles; ++j) {
+    // tiles TP*j .. TP*j+TP-1 have landed (a requesting wave waits for its own
     // requests) and every wave's reads of the previous pass are done: one
     // barrier covers both
     if (wave < 2)
-      asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"((S - 2 * KG) * kLpt) : "memory");
+      asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"((S - 2 * TP) * kLpt) : "memory");
     else
       asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     if (wave < 2) {
 #pragma unroll
-      for (int q = 0; q < KG; ++q) {
-        int sl = s0 - KG + q;
+      for (int q = 0; q < TP; ++q) {
+        int sl = s0 - TP + q;
         sl = sl < 0 ? sl + S : sl;
-        const int t_new = KG * j - KG + q + S;
+        const int t_new = TP * j - TP + q + S;
         if (wave == 0)
           dma_half_asm<D, false>(lds0 + sl * kStage, kbase, tile_row(t_new), kv_hi, lane, doff);
         else
           dma_half_asm<D, true>(lds0 + sl * kStage + kTile, vbase, tile_row(t_new), kv_hi, lane, doff);
       }
     }
-    const int t = KG * j + grp;
+#pragma unroll
+    for (int r = 0; r < TPG; ++r) {
+    const int t = TP * j + KG * r + grp;
     if (t < n_tiles) {
-      int slot = s0 + grp;
+      int slot = s0 + KG * r + grp;
       slot = slot >= S ? slot - S : slot;
       const unsigned char* kt = smem + slot * kStage;
       KTile<D> kf;
@@ -1075,7 +1080,8 @@ __global__ __launch_bounds__(512) void tree_attn_shared_kernel(AttnArgs a) {
                             plo, nbc);
       pv_bf16<D, NB, DB>(vf, 0, phi, plo, o, nbc);
     }
-    s0 += KG;
+    }
+    s0 += TP;
     s0 = s0 >= S ? s0 - S : s0;
   }
   // the DMAs past the last tile must land before the workgroup's LDS is released
@@ -1261,16 +1267,23 @@ hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int thre
   return hipErrorInvalidValue;
 }
 
+// Ring forms (slots, key groups, tiles per group and pass): one key group takes
+// three tiles per pass from ten slots, two key groups one tile each from eight.
 template <int D>
 static hipError_t shared_ring(int stages, int kg, bool launch, dim3 grid, int threads, size_t lds, const AttnArgs& a,
                               hipStream_t s, hipEvent_t ev_start) {
   const void* f = nullptr;
-  if (stages == 8 && kg == 1) f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, 8, 1>);
-  if (stages == 8 && kg == 2) f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, 8, 2>);
+  if (stages == kSharedStages1 && kg == 1)
+    f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, kSharedStages1, 1, 3>);
+  if (stages == kSharedStages2 && kg == 2)
+    f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, kSharedStages2, 2, 1>);
   if (!f) return hipErrorInvalidValue;
   if (!launch) return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (kg == 1) return launch_k(tree_attn_shared_kernel<D, 2, 8, 1>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
-  return launch_k(tree_attn_shared_kernel<D, 2, 8, 2>, grid, dim3(threads), lds, s, ev_start, nullptr, a);
+  if (kg == 1)
+    return launch_k(tree_attn_shared_kernel<D, 2, kSharedStages1, 1, 3>, grid, dim3(threads), lds, s, ev_start,
+                    nullptr, a);
+  return launch_k(tree_attn_shared_kernel<D, 2, kSharedStages2, 2, 1>, grid, dim3(threads), lds, s, ev_start, nullptr,
+                  a);
 }
 
 hipError_t launch_tree_attn_shared(int head_dim, int nb, int stages, int kg, dim3 grid, int threads, size_t lds,
