@@ -1268,7 +1268,7 @@ hipError_t launch_tree_attn(int dtype, int head_dim, int nb, dim3 grid, int thre
 }
 
 // Ring forms (slots, key groups, tiles per group and pass): one key group takes
-// three tiles per pass from ten slots, two key groups one tile each from eight.
+// three tiles per pass, two key groups two tiles each, from ten slots.
 template <int D>
 static hipError_t shared_ring(int stages, int kg, bool launch, dim3 grid, int threads, size_t lds, const AttnArgs& a,
                               hipStream_t s, hipEvent_t ev_start) {
@@ -1276,13 +1276,13 @@ static hipError_t shared_ring(int stages, int kg, bool launch, dim3 grid, int th
   if (stages == kSharedStages1 && kg == 1)
     f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, kSharedStages1, 1, 3>);
   if (stages == kSharedStages2 && kg == 2)
-    f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, kSharedStages2, 2, 1>);
+    f = reinterpret_cast<const void*>(&tree_attn_shared_kernel<D, 2, kSharedStages2, 2, 2>);
   if (!f) return hipErrorInvalidValue;
   if (!launch) return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (kg == 1)
     return launch_k(tree_attn_shared_kernel<D, 2, kSharedStages1, 1, 3>, grid, dim3(threads), lds, s, ev_start,
                     nullptr, a);
-  return launch_k(tree_attn_shared_kernel<D, 2, kSharedStages2, 2, 1>, grid, dim3(threads), lds, s, ev_start, nullptr,
+  return launch_k(tree_attn_shared_kernel<D, 2, kSharedStages2, 2, 2>, grid, dim3(threads), lds, s, ev_start, nullptr,
                   a);
 }
 

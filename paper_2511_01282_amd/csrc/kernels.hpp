@@ -128,7 +128,7 @@ hipError_t launch_tree_attn_shared(int head_dim, int nb, int stages, int kg, dim
 hipError_t set_tree_attn_shared_lds_limit(int head_dim, int stages, int kg, size_t lds);
 constexpr int shared_ring_bytes(int head_dim, int stages) { return stages * 2 * kKvTile * head_dim * 2; }
 constexpr int kSharedStages1 = 10;  // ring slots of the shared-tile kernel with one key group (160 KB at head_dim 128)
-constexpr int kSharedStages2 = 8;   // ... and with two key groups
+constexpr int kSharedStages2 = 10;  // ... and with two key groups
 // mb: 16-row token blocks per workgroup (1-4 plain, 8 or 16 tiled); wide: bf16 with up to 64 token rows
 // in 256-row vocabulary tiles (n_mtiles = 1)
 hipError_t launch_lmhead(int dtype, int mb, bool wide, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
