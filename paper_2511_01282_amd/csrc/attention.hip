@@ -17,7 +17,10 @@
 //     the matrix cores; bf16 P is split into hi + lo bf16 parts so that the
 //     probabilities keep ~16 significant bits (bf16 P alone perturbs x enough
 //     to move logits by ~5e-4);
-//   - each wave keeps two KV tiles in flight while it processes a third;
+//   - each wave keeps two KV tiles in flight while it processes a third (with
+//     several waves of rows per KV head, bf16: the waves instead share KV
+//     tiles that a DMA ring brings into LDS, several tiles per barrier; see
+//     the shared-tile variant below);
 //   - waves of a row group are merged in LDS; each workgroup writes an
 //     unnormalised partial (O, max, sum) per row;
 //   - a second, wide kernel merges the splits of every row and writes O and
