@@ -585,19 +585,26 @@ __global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
 //   - stage rows are 128 bytes with chunk c of row r stored at chunk position
 //     c ^ ((r >> 1) & 7): a quarter-wave reading one chunk of 16 consecutive
 //     rows touches all 64 banks once;
+//   - eight waves (two per SIMD) in a 2 x 4 grid: wave w owns vocabulary rows
+//     64 (w & 1) .. +63 and token rows MT/4 (w >> 1) .. +MT/4-1, and issues an
+//     eighth of every step's DMA requests (four waves in a 2 x 2 grid, each
+//     with twice the products and requests, measured ~6 % slower: the CU's
+//     feed from L2 grows with the number of waves that issue);
 //   - products on v_mfma_f32_32x32x16_bf16 with W as the A operand (32
-//     vocabulary rows) and x as the B operand (32 token rows); wave w owns
-//     vocabulary rows 64 (w & 1) .. +63 and token rows MT/2 (w >> 1) .. +MT/2-1;
-//     each step's fragments are requested ahead of its products;
+//     vocabulary rows) and x as the B operand (32 token rows); each step's
+//     fragments are requested ahead of its products;
 //   - a lane's accumulator holds, for token row (lane & 31) of a block, the
 //     vocabulary rows 8 g + 4 (lane >> 5) + e (g, e = 0..3) of a 32-row block;
 //   - the logits leave through LDS as a [token row][128] tile, so that each
-//     token row's 512 bytes are stored contiguously, and each thread reduces
-//     one token row of that tile to its two statistics tiles.
+//     token row's 512 bytes are stored contiguously, and each of the first
+//     MT threads reduces one token row of that tile to its two statistics
+//     tiles.
 constexpr int kGmVRows = 128;                   // vocabulary rows per workgroup
 constexpr int kGmTileRowB = kGmVRows * 4 + 16;  // LDS row stride of the logit tile (bytes)
 
 constexpr int kGmStep = 128;                    // bytes of a row per K step (64 elements)
+constexpr int kGmWT = 4;                        // token quarters of the wave grid
+constexpr int kGmWaves = 2 * kGmWT;             // waves per workgroup
 
 template <int MT>
 struct GmShape {
@@ -606,12 +613,14 @@ struct GmShape {
   static constexpr int KS = kGmStep / 32;                           // 16-element slices per step
   static constexpr int kStage = (MT + kGmVRows) * kGmStep;          // bytes per stage
   static constexpr int S = 147456 / kStage;                         // stages (144 KB of LDS)
-  static constexpr int kXInst = MT / RPI / 4;                       // x DMA requests per wave per step
-  static constexpr int kWInst = kGmVRows / RPI / 4;                 // W DMA requests per wave per step
+  static constexpr int kXInst = MT / RPI / kGmWaves;                // x DMA requests per wave per step
+  static constexpr int kWInst = kGmVRows / RPI / kGmWaves;          // W DMA requests per wave per step
   static constexpr int kPerStep = kXInst + kWInst;
-  static constexpr int NT = MT / 2 / 32;                            // 32-row token blocks per wave
+  static constexpr int NT = MT / kGmWT / 32;                        // 32-row token blocks per wave
   static constexpr int kLds = S * kStage > MT * kGmTileRowB ? S * kStage : MT * kGmTileRowB;
   static_assert(S >= 3 && (S - 1) * kPerStep <= 63, "stages and memory counter range");
+  static_assert(MT % (RPI * kGmWaves) == 0 && kGmVRows % (RPI * kGmWaves) == 0 && MT % (kGmWT * 32) == 0,
+                "every wave issues whole DMA requests and owns whole 32-row token blocks");
   // chunk position of chunk c of stage row r
   static __device__ __forceinline__ int swz(int c, int r) { return c ^ ((r >> 1) & 7); }
 };
@@ -637,7 +646,7 @@ __device__ __forceinline__ uint64_t uniform_u64(uint64_t v) {
 }
 
 template <int MT>
-__global__ __launch_bounds__(256) void lmhead_gemm_kernel(LmArgs a) {
+__global__ __launch_bounds__(64 * kGmWaves) void lmhead_gemm_kernel(LmArgs a) {
   using G = GmShape<MT>;
   typedef float f32x16 __attribute__((ext_vector_type(16)));
   __shared__ __align__(1024) unsigned char sm[G::kLds];
@@ -696,7 +705,7 @@ __global__ __launch_bounds__(256) void lmhead_gemm_kernel(LmArgs a) {
 #pragma unroll
   for (int ks = 0; ks < G::KS; ++ks) kof[ks] = (uint32_t)(r32 * kGmStep + G::swz(2 * ks + hi, r32) * 16);
   const int a_row0 = MT + 64 * wv;     // stage row of the wave's first W row
-  const int b_row0 = wt * (MT / 2);    // stage row of the wave's first x row
+  const int b_row0 = wt * (MT / kGmWT);  // stage row of the wave's first x row
 
   f32x16 acc[2][G::NT];
 #pragma unroll
@@ -766,7 +775,7 @@ __global__ __launch_bounds__(256) void lmhead_gemm_kernel(LmArgs a) {
     const bool vec_ok = (a.vocab & 3) == 0;
     const int col = 4 * r32;  // this lane's 4 vocabulary rows of a token row
     const int vv = v0 + col;
-    for (int row = 2 * wave + hi; row < rows; row += 8) {  // two token rows per wave and pass
+    for (int row = 2 * wave + hi; row < rows; row += 2 * kGmWaves) {  // two token rows per wave and pass
       const f32x4 q = *reinterpret_cast<const f32x4*>(tile + row * kGmTileRowB + col * 4);
       float* dst = a.logits + (size_t)(m0 + row) * a.vocab + vv;
       if (vec_ok && vv + 3 < a.vocab) {
@@ -780,8 +789,8 @@ __global__ __launch_bounds__(256) void lmhead_gemm_kernel(LmArgs a) {
   }
   if (!a.partials) return;
 
-  // statistics: thread t reduces token row t (and t + 256) over each 64-row statistics tile
-  for (int row = threadIdx.x; row < rows; row += 256) {
+  // statistics: thread t < MT reduces token row t over each 64-row statistics tile
+  for (int row = threadIdx.x; row < rows; row += 64 * kGmWaves) {
 #pragma unroll
     for (int h = 0; h < kGmVRows / kLmTileRows; ++h) {
       const int vh = v0 + kLmTileRows * h;
@@ -872,7 +881,7 @@ hipError_t launch_lmhead(int dtype, int mb, bool wide, const LmArgs& a, hipStrea
     if (dtype != 1 || a.hidden_size % 256 != 0) return hipErrorInvalidValue;
     const int n_vt2 = (a.vocab + kGmVRows - 1) / kGmVRows;
     dim3 tgrid(((n_vt2 + 7) / 8) * 8 * a.n_mtiles);
-    return launch_k(lmhead_gemm_kernel<256>, tgrid, dim3(256), 0, s, nullptr, ev_stop, a);
+    return launch_k(lmhead_gemm_kernel<256>, tgrid, dim3(64 * kGmWaves), 0, s, nullptr, ev_stop, a);
   }
   if (wide) {  // wide tiled variant: up to 64 token rows, 256-row vocabulary tiles (bf16)
     if (dtype != 1 || mb > 4) return hipErrorInvalidValue;
