@@ -365,12 +365,10 @@ __global__ __launch_bounds__(256, 2) void lmhead_persistent_kernel(LmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Tiled variant (bf16) for many token rows (65 to 256 per pass, 128
-// vocabulary rows per workgroup) and for large vocabularies with up to 64
-// token rows (256 vocabulary rows per workgroup).  There the x rows a
-// workgroup pulls through its CU weigh as much as W or more, so a workgroup
-// owns 16*NVB vocabulary rows (NVB/4 statistics tiles), and every byte of W
-// and x it needs crosses the CU once per pass:
+// Tiled variant (bf16) for 65 to 128 token rows (128 vocabulary rows per
+// workgroup).  There the x rows a workgroup pulls through its CU weigh as
+// much as W, so a workgroup owns 16*NVB vocabulary rows (NVB/4 statistics
+// tiles), and every byte of W and x it needs crosses the CU once per pass:
 //   - the W rows of a K step go through a double-buffered LDS tile
 //     (requested into registers, NVB/2 pieces of 16 bytes per thread,
 //     written to LDS; one barrier per step), from which every wave reads its
@@ -572,12 +570,14 @@ __global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// GEMM variant (bf16) for tiles of 256 token rows (129 or more rows in all).
-// A workgroup owns 128 vocabulary rows and MT = 256 token rows; every byte of
-// W and x it needs crosses its CU once:
+// GEMM variant (bf16), fed by DMA, in two tile shapes: MT = 256 token rows by
+// VR = 128 vocabulary rows (129 or more rows in all), and MT = 64 by VR = 256
+// (at most 64 rows over a vocabulary of more than two 64-row tiles per CU,
+// where each x row then serves four times as many W rows).  Every byte of W
+// and x a workgroup needs crosses its CU once:
 //   - K advances in 128-byte steps (64 elements); the W and x rows of a step go
 //     straight from memory into an LDS stage by DMA (global_load_lds, 16 bytes
-//     per lane, no registers), in a ring of S = 3 stages of 48 KB: after the
+//     per lane, no registers), in a ring of S = 3 stages (48 or 40 KB): after the
 //     barrier that publishes step c (every wave has finished step c-1 by then)
 //     step c+2 is requested into c-1's stage, so two steps are in flight while
 //     one is multiplied (the W and x rows of a step share a stage: giving W a
@@ -585,41 +585,43 @@ __global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
 //   - stage rows are 128 bytes with chunk c of row r stored at chunk position
 //     c ^ ((r >> 1) & 7): a quarter-wave reading one chunk of 16 consecutive
 //     rows touches all 64 banks once;
-//   - eight waves (two per SIMD) in a 2 x 4 grid: wave w owns vocabulary rows
-//     64 (w & 1) .. +63 and token rows MT/4 (w >> 1) .. +MT/4-1, and issues an
-//     eighth of every step's DMA requests (four waves in a 2 x 2 grid, each
-//     with twice the products and requests, measured ~6 % slower: the CU's
-//     feed from L2 grows with the number of waves that issue);
+//   - eight waves (two per SIMD) in a WV x WT grid (VR/64 vocabulary waves):
+//     wave w owns vocabulary rows 64 (w % WV) .. +63 and token rows
+//     MT/WT (w / WV) .. +MT/WT-1, and issues an eighth of every step's DMA
+//     requests (at 256 x 128, four waves in a 2 x 2 grid, each with twice the
+//     products and requests, measured ~6 % slower: the CU's feed from L2 grows
+//     with the number of waves that issue);
 //   - products on v_mfma_f32_32x32x16_bf16 with W as the A operand (32
 //     vocabulary rows) and x as the B operand (32 token rows); each step's
 //     fragments are requested ahead of its products;
 //   - a lane's accumulator holds, for token row (lane & 31) of a block, the
 //     vocabulary rows 8 g + 4 (lane >> 5) + e (g, e = 0..3) of a 32-row block;
 //   - the logits leave through LDS as a [token row][128] tile, so that each
-//     token row's 512 bytes are stored contiguously, and each of the first
-//     MT threads reduces one token row of that tile to its two statistics
-//     tiles.
-constexpr int kGmVRows = 128;                   // vocabulary rows per workgroup
-constexpr int kGmTileRowB = kGmVRows * 4 + 16;  // LDS row stride of the logit tile (bytes)
-
+//     token row's 4 VR bytes are stored contiguously, and each thread reduces
+//     one token row of that tile over one 64-row statistics tile.
 constexpr int kGmStep = 128;                    // bytes of a row per K step (64 elements)
-constexpr int kGmWT = 4;                        // token quarters of the wave grid
-constexpr int kGmWaves = 2 * kGmWT;             // waves per workgroup
+constexpr int kGmWaves = 8;                     // waves per workgroup
 
-template <int MT>
+template <int MT, int VR>
 struct GmShape {
+  static constexpr int WV = VR / 64;                                // vocabulary waves (64 rows each)
+  static constexpr int WT = kGmWaves / WV;                          // token waves
   static constexpr int CPR = kGmStep / 16;                          // 16-byte chunks per stage row
   static constexpr int RPI = 64 / CPR;                              // stage rows per DMA request
   static constexpr int KS = kGmStep / 32;                           // 16-element slices per step
-  static constexpr int kStage = (MT + kGmVRows) * kGmStep;          // bytes per stage
+  static constexpr int kStage = (MT + VR) * kGmStep;                // bytes per stage
   static constexpr int S = 147456 / kStage;                         // stages (144 KB of LDS)
   static constexpr int kXInst = MT / RPI / kGmWaves;                // x DMA requests per wave per step
-  static constexpr int kWInst = kGmVRows / RPI / kGmWaves;          // W DMA requests per wave per step
+  static constexpr int kWInst = VR / RPI / kGmWaves;                // W DMA requests per wave per step
   static constexpr int kPerStep = kXInst + kWInst;
-  static constexpr int NT = MT / kGmWT / 32;                        // 32-row token blocks per wave
-  static constexpr int kLds = S * kStage > MT * kGmTileRowB ? S * kStage : MT * kGmTileRowB;
+  static constexpr int NT = MT / WT / 32;                           // 32-row token blocks per wave
+  static constexpr int kTileRowB = VR * 4 + 16;                     // LDS row stride of the logit tile
+  static constexpr int kLds = S * kStage > MT * kTileRowB ? S * kStage : MT * kTileRowB;
+  static constexpr int LPR = VR / 4;                                // lanes per token row of the store
+  static constexpr int kStats = VR / kLmTileRows;                   // statistics tiles per token row
   static_assert(S >= 3 && (S - 1) * kPerStep <= 63, "stages and memory counter range");
-  static_assert(MT % (RPI * kGmWaves) == 0 && kGmVRows % (RPI * kGmWaves) == 0 && MT % (kGmWT * 32) == 0,
+  static_assert(VR % 64 == 0 && kGmWaves % WV == 0 && 64 % LPR == 0, "wave grid and store shape");
+  static_assert(MT % (RPI * kGmWaves) == 0 && VR % (RPI * kGmWaves) == 0 && MT % (WT * 32) == 0,
                 "every wave issues whole DMA requests and owns whole 32-row token blocks");
   // chunk position of chunk c of stage row r
   static __device__ __forceinline__ int swz(int c, int r) { return c ^ ((r >> 1) & 7); }
@@ -645,9 +647,9 @@ __device__ __forceinline__ uint64_t uniform_u64(uint64_t v) {
          (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
 }
 
-template <int MT>
+template <int MT, int VR>
 __global__ __launch_bounds__(64 * kGmWaves) void lmhead_gemm_kernel(LmArgs a) {
-  using G = GmShape<MT>;
+  using G = GmShape<MT, VR>;
   typedef float f32x16 __attribute__((ext_vector_type(16)));
   __shared__ __align__(1024) unsigned char sm[G::kLds];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)sm;
@@ -659,8 +661,8 @@ __global__ __launch_bounds__(64 * kGmWaves) void lmhead_gemm_kernel(LmArgs a) {
   const int id = blockIdx.x;
   const int grp = id / (8 * n_mt), rem = id % (8 * n_mt);
   const int vt = grp * 8 + rem % 8, mt = rem / 8;  // the M tiles of a vocabulary tile share an XCD
-  if (vt * kGmVRows >= a.vocab) return;
-  const int v0 = vt * kGmVRows;
+  if (vt * VR >= a.vocab) return;
+  const int v0 = vt * VR;
   const int m0 = mt * MT;
   const size_t row_bytes = (size_t)a.hidden_size * 2;
   const int n_steps = (int)(row_bytes / kGmStep);  // >= 4 (hidden*2 is a multiple of 512; checked)
@@ -699,13 +701,13 @@ __global__ __launch_bounds__(64 * kGmWaves) void lmhead_gemm_kernel(LmArgs a) {
              wo[j]);
   };
 
-  const int wv = wave & 1, wt = wave >> 1;
+  const int wv = wave % G::WV, wt = wave / G::WV;
   // LDS byte offsets of this lane's fragments within a 32-row block, per 16-element slice
   uint32_t kof[G::KS];
 #pragma unroll
   for (int ks = 0; ks < G::KS; ++ks) kof[ks] = (uint32_t)(r32 * kGmStep + G::swz(2 * ks + hi, r32) * 16);
   const int a_row0 = MT + 64 * wv;     // stage row of the wave's first W row
-  const int b_row0 = wt * (MT / kGmWT);  // stage row of the wave's first x row
+  const int b_row0 = wt * (MT / G::WT);  // stage row of the wave's first x row
 
   f32x16 acc[2][G::NT];
 #pragma unroll
@@ -758,7 +760,7 @@ __global__ __launch_bounds__(64 * kGmWaves) void lmhead_gemm_kernel(LmArgs a) {
 
   // logits through LDS: the stages are free once every wave has finished the last step
   __syncthreads();
-  unsigned char* tile = sm;  // [MT][kGmTileRowB] bytes
+  unsigned char* tile = sm;  // [MT][kTileRowB] bytes
 #pragma unroll
   for (int n = 0; n < G::NT; ++n)
 #pragma unroll
@@ -766,17 +768,18 @@ __global__ __launch_bounds__(64 * kGmWaves) void lmhead_gemm_kernel(LmArgs a) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int row = b_row0 + 32 * n + r32, col = 64 * wv + 32 * i + 8 * g + 4 * hi;
-        *reinterpret_cast<f32x4*>(tile + row * kGmTileRowB + col * 4) =
+        *reinterpret_cast<f32x4*>(tile + row * G::kTileRowB + col * 4) =
             f32x4{acc[i][n][4 * g], acc[i][n][4 * g + 1], acc[i][n][4 * g + 2], acc[i][n][4 * g + 3]};
       }
   __syncthreads();
   const int rows = min(MT, a.m_rows - m0);
   {
     const bool vec_ok = (a.vocab & 3) == 0;
-    const int col = 4 * r32;  // this lane's 4 vocabulary rows of a token row
+    constexpr int kRowsPerWave = 64 / G::LPR;  // token rows a wave stores per pass
+    const int col = 4 * (lane % G::LPR);        // this lane's 4 vocabulary rows of a token row
     const int vv = v0 + col;
-    for (int row = 2 * wave + hi; row < rows; row += 2 * kGmWaves) {  // two token rows per wave and pass
-      const f32x4 q = *reinterpret_cast<const f32x4*>(tile + row * kGmTileRowB + col * 4);
+    for (int row = kRowsPerWave * wave + lane / G::LPR; row < rows; row += kRowsPerWave * kGmWaves) {
+      const f32x4 q = *reinterpret_cast<const f32x4*>(tile + row * G::kTileRowB + col * 4);
       float* dst = a.logits + (size_t)(m0 + row) * a.vocab + vv;
       if (vec_ok && vv + 3 < a.vocab) {
         *reinterpret_cast<f32x4*>(dst) = q;
@@ -789,13 +792,13 @@ __global__ __launch_bounds__(64 * kGmWaves) void lmhead_gemm_kernel(LmArgs a) {
   }
   if (!a.partials) return;
 
-  // statistics: thread t < MT reduces token row t over each 64-row statistics tile
-  for (int row = threadIdx.x; row < rows; row += 64 * kGmWaves) {
-#pragma unroll
-    for (int h = 0; h < kGmVRows / kLmTileRows; ++h) {
+  // statistics: one (token row, 64-row statistics tile) pair per thread and pass
+  for (int u = threadIdx.x; u < MT * G::kStats; u += 64 * kGmWaves) {
+    {
+      const int row = u % MT, h = u / MT;
       const int vh = v0 + kLmTileRows * h;
-      if (vh >= a.vocab) break;  // (no statistics tile past V)
-      const unsigned char* zr = tile + row * kGmTileRowB + h * kLmTileRows * 4;
+      if (row >= rows || vh >= a.vocab) continue;  // (no statistics tile past V)
+      const unsigned char* zr = tile + row * G::kTileRowB + h * kLmTileRows * 4;
       float z[kLmTileRows];
 #pragma unroll
       for (int q = 0; q < kLmTileRows / 4; ++q) {
@@ -879,15 +882,15 @@ hipError_t launch_lmhead(int dtype, int mb, bool wide, const LmArgs& a, hipStrea
   }
   if (mb == 16) {  // GEMM variant: 256 token rows per tile, 128-row vocabulary tiles (bf16)
     if (dtype != 1 || a.hidden_size % 256 != 0) return hipErrorInvalidValue;
-    const int n_vt2 = (a.vocab + kGmVRows - 1) / kGmVRows;
+    const int n_vt2 = (a.vocab + 127) / 128;
     dim3 tgrid(((n_vt2 + 7) / 8) * 8 * a.n_mtiles);
-    return launch_k(lmhead_gemm_kernel<256>, tgrid, dim3(64 * kGmWaves), 0, s, nullptr, ev_stop, a);
+    return launch_k(lmhead_gemm_kernel<256, 128>, tgrid, dim3(64 * kGmWaves), 0, s, nullptr, ev_stop, a);
   }
-  if (wide) {  // wide tiled variant: up to 64 token rows, 256-row vocabulary tiles (bf16)
-    if (dtype != 1 || mb > 4) return hipErrorInvalidValue;
+  if (wide) {  // GEMM variant: up to 64 token rows, 256-row vocabulary tiles (bf16)
+    if (dtype != 1 || mb > 4 || a.hidden_size % 256 != 0) return hipErrorInvalidValue;
     const int n_vt2 = (a.vocab + 255) / 256;
     dim3 tgrid(((n_vt2 + 7) / 8) * 8 * a.n_mtiles);
-    return launch_k(lmhead_tiled_kernel<1, 16>, tgrid, dim3(256), 0, s, nullptr, ev_stop, a);
+    return launch_k(lmhead_gemm_kernel<64, 256>, tgrid, dim3(64 * kGmWaves), 0, s, nullptr, ev_stop, a);
   }
   return dtype == 1 ? launch_mb<bf16_t>(mb, grid, a, s, ev_stop) : launch_mb<float>(mb, grid, a, s, ev_stop);
 }

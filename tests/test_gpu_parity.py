@@ -234,6 +234,7 @@ VOCAB_TIERS = [
     (30000, 8, "clustered"),
     (30000, 16, "tied"),
     (70000, 8, "plain"),
+    (40001, 8, "plain"),       # 256-row vocabulary tiles with a ragged last tile and unaligned logit rows
     (200000, 16, "clustered"),
     (300000, 8, "clustered"),
 ]
