@@ -596,7 +596,7 @@ __global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
 //     fragments are requested ahead of its products;
 //   - a lane's accumulator holds, for token row (lane & 31) of a block, the
 //     vocabulary rows 8 g + 4 (lane >> 5) + e (g, e = 0..3) of a 32-row block;
-//   - the logits leave through LDS as a [token row][128] tile, so that each
+//   - the logits leave through LDS as a [token row][VR] tile, so that each
 //     token row's 4 VR bytes are stored contiguously, and each thread reduces
 //     one token row of that tile over one 64-row statistics tile.
 constexpr int kGmStep = 128;                    // bytes of a row per K step (64 elements)
