@@ -240,6 +240,24 @@ VOCAB_TIERS = [
 ]
 
 
+# At most 64 token rows over a vocabulary of more than two 64-row tiles per CU
+# take the LM head's 64 x 256 tile: one row (every other x row a clamped copy),
+# a partial tile and a full one, over a vocabulary that is a multiple of neither
+# 4 nor 256 (unaligned logit rows, a ragged last tile).
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("n_nodes", [1, 33, 64])
+def test_wide_vocab_token_rows(rt, n_nodes):
+    vocab = 33001
+    parents = [[-1] + [(j - 1) // 2 for j in range(1, n_nodes)]]
+    depth = max(8, _depth(parents[0]))
+    shp = synth.Shape("edge", "bf16", 4 * 64, 4, 2, 64, vocab, 1, n_nodes, depth, 8)
+    w = synth.custom(shp, parents, [150], seed=233 + n_nodes, poison_tail=True)
+    _say(f"[wide vocab {vocab}, {n_nodes} rows] building")
+    case = workload.finish(w)
+    _say(f"[wide vocab {vocab}, {n_nodes} rows] running GPU step")
+    compare(case, rt.run(case.w, x_out=True, tok_rank=True), f"wide vocab {n_nodes} rows")
+
+
 @pytest.mark.timeout(300)
 @pytest.mark.parametrize("vocab,topk_out,mode", VOCAB_TIERS)
 def test_vocab_tier_parity(rt, vocab, topk_out, mode):
