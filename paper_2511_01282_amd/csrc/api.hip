@@ -310,9 +310,8 @@ respec_status step_impl(const respec_verify_plan* plan, const respec_verify_args
     lm.m_rows = a.total_nodes;
     lm.vocab = s.vocab;
     lm.hidden_size = s.hidden;
-    // token rows per workgroup 16*mb: up to 64 in the plain kernel, 128 in the
-    // tiled one and 256 in the GEMM one (bf16), so that W is streamed once for
-    // up to 256 rows.  A vocabulary of more 64-row tiles than two per CU takes
+    // token rows per workgroup 16*mb: up to 64 in the plain kernel, 128 or 256
+    // in the GEMM one (bf16), so that W is streamed once for up to 256 rows.  A vocabulary of more 64-row tiles than two per CU takes
     // the GEMM kernel's 256-row vocabulary tiles (bf16): each x row then serves
     // four times as many W rows.
     const int M = a.total_nodes;

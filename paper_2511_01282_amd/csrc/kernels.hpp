@@ -129,7 +129,7 @@ hipError_t set_tree_attn_shared_lds_limit(int head_dim, int stages, int kg, size
 constexpr int shared_ring_bytes(int head_dim, int stages) { return stages * 2 * kKvTile * head_dim * 2; }
 constexpr int kSharedStages1 = 10;  // ring slots of the shared-tile kernel with one key group (160 KB at head_dim 128)
 constexpr int kSharedStages2 = 10;  // ... and with two key groups
-// mb: 16-row token blocks per workgroup (1-4 plain, 8 tiled, 16 GEMM); wide: bf16 with up to 64 token
+// mb: 16-row token blocks per workgroup (1-4 plain, 8 and 16 GEMM); wide: bf16 with up to 64 token
 // rows in the GEMM kernel's 256-row vocabulary tiles (n_mtiles = 1)
 hipError_t launch_lmhead(int dtype, int mb, bool wide, const LmArgs& a, hipStream_t s, hipEvent_t ev_stop = nullptr);
 constexpr int kLmTileRows = 64;  // vocabulary rows per statistics tile (one plain LM-head workgroup)

@@ -365,216 +365,12 @@ __global__ __launch_bounds__(256, 2) void lmhead_persistent_kernel(LmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Tiled variant (bf16) for 65 to 128 token rows (128 vocabulary rows per
-// workgroup).  There the x rows a workgroup pulls through its CU weigh as
-// much as W, so a workgroup owns 16*NVB vocabulary rows (NVB/4 statistics
-// tiles), and every byte of W and x it needs crosses the CU once per pass:
-//   - the W rows of a K step go through a double-buffered LDS tile
-//     (requested into registers, NVB/2 pieces of 16 bytes per thread,
-//     written to LDS; one barrier per step), from which every wave reads its
-//     A fragments;
-//   - wave w owns token rows 16*TB*w .. +16*TB-1 and requests its x fragments
-//     (the B operands) straight into registers; token blocks past the last
-//     row are not multiplied;
-//   - K advances in 128-byte steps through a ring of four register stages:
-//     step c is consumed while steps c+1 .. c+3 are in flight, and step c+4
-//     is requested into the freed registers right after step c's products;
-//   - each wave reduces its token rows over each 64-row quarter of the tile
-//     to the per-tile statistics.
-constexpr int kTlStep = 128;                 // bytes of a row per K step
-constexpr int kTlPieces = kTlStep / 64;      // mma_k64 calls per K step
-constexpr int kTlWStride = kTlStep + 16;     // LDS row stride of the W tile
-constexpr int kTlRing = 4;                   // register stages
-
-template <int TB, int NVB>
-__device__ __forceinline__ void lmhead_tiled_body(const LmArgs& a) {
-  constexpr int VB = NVB;                           // 16-row vocabulary blocks (all waves)
-  constexpr int kTlRows = 16 * NVB;                 // vocabulary rows per workgroup
-  constexpr int MT = 64 * TB;                       // token rows per workgroup
-  constexpr int WP = kTlRows * kTlStep / 16 / 256;  // 16-byte W pieces per thread per step
-  constexpr int NS = kTlRows / kLmTileRows;         // statistics tiles per workgroup
-  __shared__ __align__(16) unsigned char sw[2 * kTlRows * kTlWStride];
-
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int lr = lane & 15, lg = lane >> 4;
-  const int n_mt = a.n_mtiles;
-  const int id = blockIdx.x;
-  const int grp = id / (8 * n_mt), rem = id % (8 * n_mt);
-  const int vt = grp * 8 + rem % 8, mt = rem / 8;  // vt: tile of kTlRows vocabulary rows
-  if (vt * kTlRows >= a.vocab) return;
-  const int v0 = vt * kTlRows;                     // first vocabulary row of the workgroup
-  const int m0 = mt * MT + 16 * TB * wave;         // first token row of this wave
-  // (uniform per wave) token blocks of this wave that hold a row
-  const int tbl = __builtin_amdgcn_readfirstlane(min(TB, max(0, (a.m_rows - m0 + 15) / 16)));
-  const size_t row_bytes = (size_t)a.hidden_size * 2;
-  const int n_steps = (int)(row_bytes / kTlStep);  // >= 4 (hidden*2 is a multiple of 512)
-  const int rot = vt % n_steps;                    // per-workgroup K start (spreads the channels)
-  auto step_of = [&](int c) { return c + rot < n_steps ? c + rot : c + rot - n_steps; };
-
-  const char* wpiece[WP];
-#pragma unroll
-  for (int q = 0; q < WP; ++q) {
-    const int pidx = threadIdx.x + 256 * q;
-    const int r = pidx / (kTlStep / 16), pc = pidx % (kTlStep / 16);
-    const int v = min(v0 + r, a.vocab - 1);  // rows past V: a valid row, results not stored
-    wpiece[q] = reinterpret_cast<const char*>(a.w) + (size_t)v * row_bytes + pc * 16;
-  }
-  const char* xrow[TB];
-#pragma unroll
-  for (int tb = 0; tb < TB; ++tb) {
-    const int m = min(m0 + 16 * tb + lr, a.m_rows - 1);  // rows past M: a valid row, results not stored
-    xrow[tb] = reinterpret_cast<const char*>(a.x) + (size_t)m * row_bytes + lg * 16;
-  }
-
-  struct Stage {
-    u32x4 w[WP];
-    u32x4 x[TB][kTlPieces];
-  };
-  auto issue = [&](Stage& st, int c) {
-    const size_t off = (size_t)step_of(c) * kTlStep;
-#pragma unroll
-    for (int q = 0; q < WP; ++q) st.w[q] = ld16(wpiece[q] + off);
-    // (every block is requested, so that each stage holds the same count of
-    // requests; a block past the last row reads row M-1 in every lane, one
-    // cache line per request)
-#pragma unroll
-    for (int tb = 0; tb < TB; ++tb)
-#pragma unroll
-      for (int kp = 0; kp < kTlPieces; ++kp) st.x[tb][kp] = ld16(xrow[tb] + off + kp * 64);
-  };
-  auto stage_w = [&](const Stage& st, unsigned char* buf) {
-#pragma unroll
-    for (int q = 0; q < WP; ++q) {
-      const int pidx = threadIdx.x + 256 * q;
-      const int r = pidx / (kTlStep / 16), pc = pidx % (kTlStep / 16);
-      *reinterpret_cast<u32x4*>(buf + r * kTlWStride + pc * 16) = st.w[q];
-    }
-  };
-
-  f32x4 acc[VB][TB];
-#pragma unroll
-  for (int vb = 0; vb < VB; ++vb)
-#pragma unroll
-    for (int tb = 0; tb < TB; ++tb) acc[vb][tb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  auto mma_step = [&](const Stage& st, const unsigned char* buf) {
-#pragma unroll
-    for (int kp = 0; kp < kTlPieces; ++kp)
-#pragma unroll
-      for (int v0b = 0; v0b < VB; v0b += 8) {  // 8 A fragments at a time
-        u32x4 wf[8];
-#pragma unroll
-        for (int vb = 0; vb < 8; ++vb)
-          wf[vb] = *reinterpret_cast<const u32x4*>(buf + (16 * (v0b + vb) + lr) * kTlWStride + kp * 64 + lg * 16);
-#pragma unroll
-        for (int tb = 0; tb < TB; ++tb)
-          if (tb < tbl)
-#pragma unroll
-            for (int vb = 0; vb < 8; ++vb)
-              acc[v0b + vb][tb] = mma_k64(bf16_t{}, wf[vb], st.x[tb][kp], acc[v0b + vb][tb]);
-      }
-  };
-
-  // The steady-state loop only refills real steps (the same count of requests
-  // behind every step on every pass); the last steps (straight-line code)
-  // refill while steps remain, so nothing is in flight at the epilogue.  W
-  // alternates between two LDS buffers (the barrier of step c+1 orders step
-  // c's reads before the writes of step c+2).
-  Stage ring[kTlRing];
-#pragma unroll
-  for (int j = 0; j < kTlRing; ++j) {
-    issue(ring[j], min(j, n_steps - 1));
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  auto step = [&](Stage& st, int c, bool refill) {
-    unsigned char* buf = sw + (c & 1) * kTlRows * kTlWStride;
-    stage_w(st, buf);
-    __syncthreads();
-    mma_step(st, buf);
-    if (refill) issue(st, c + kTlRing);
-    __builtin_amdgcn_sched_barrier(0);  // keep the requests here, ahead of the next step's wait
-  };
-  int c = 0;
-  for (; c + 2 * kTlRing <= n_steps; c += kTlRing) {
-#pragma unroll
-    for (int j = 0; j < kTlRing; ++j) step(ring[j], c + j, true);
-  }
-#pragma unroll
-  for (int j = 0; j < 2 * kTlRing - 1; ++j)
-    if (c + j < n_steps) step(ring[j % kTlRing], c + j, c + j + kTlRing < n_steps);
-
-  // logits: lane holds z[m0 + 16*tb + lr][v0 + 16*vb + 4*lg + i]
-  const bool vec_ok = (a.vocab & 3) == 0;
-#pragma unroll
-  for (int tb = 0; tb < TB; ++tb) {
-    const int m = m0 + 16 * tb + lr;
-    if (tb >= tbl || m >= a.m_rows) continue;
-#pragma unroll
-    for (int vb = 0; vb < VB; ++vb) {
-      const int vv = v0 + 16 * vb + 4 * lg;
-      float* dst = a.logits + (size_t)m * a.vocab + vv;
-      if (vec_ok && vv + 3 < a.vocab) {
-        *reinterpret_cast<f32x4*>(dst) = acc[vb][tb];
-      } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (vv + i < a.vocab) dst[i] = acc[vb][tb][i];
-      }
-    }
-  }
-  if (!a.partials) return;
-
-  // per-tile statistics of each token row over each 64-row quarter of the tile
-#pragma unroll
-  for (int half = 0; half < NS; ++half) {
-    const int vh = v0 + 64 * half;
-    if (vh >= a.vocab) break;  // (no statistics tile past V)
-#pragma unroll
-    for (int tb = 0; tb < TB; ++tb) {
-      if (tb >= tbl) continue;
-      float mx = kNegInf;
-#pragma unroll
-      for (int vb = 4 * half; vb < 4 * half + 4; ++vb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int col = v0 + 16 * vb + 4 * lg + i;
-          mx = col < a.vocab ? fmaxf(mx, acc[vb][tb][i]) : mx;
-        }
-      RowStats st;
-      st.init();
-      st.m = mx;
-#pragma unroll
-      for (int vb = 4 * half; vb < 4 * half + 4; ++vb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int col = v0 + 16 * vb + 4 * lg + i;
-          const bool ok = col < a.vocab;
-          const float d = acc[vb][tb][i] - mx;
-          const float e = ok ? __expf(d) : 0.f;
-          st.S += e;
-          st.T += ok ? e * d : 0.f;
-          st.am = (ok && acc[vb][tb][i] == mx) ? min(st.am, col) : st.am;
-        }
-      st.merge_level<4>();  // lane groups of a token row: xor 16, xor 32
-      st.merge_level<5>();
-      const int m = m0 + 16 * tb + lr;
-      if (lg == 0 && m < a.m_rows)
-        *reinterpret_cast<u32x4*>(a.partials + ((size_t)m * a.n_vtiles + NS * vt + half) * kTileWords) =
-            u32x4{__float_as_uint(st.m), __float_as_uint(st.S), __float_as_uint(st.T), (uint32_t)st.am};
-    }
-  }
-}
-
-template <int TB, int NVB>
-__global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
-  lmhead_tiled_body<TB, NVB>(a);
-}
-
-// ---------------------------------------------------------------------------
-// GEMM variant (bf16), fed by DMA, in two tile shapes: MT = 256 token rows by
-// VR = 128 vocabulary rows (129 or more rows in all), and MT = 64 by VR = 256
-// (at most 64 rows over a vocabulary of more than two 64-row tiles per CU,
-// where each x row then serves four times as many W rows).  Every byte of W
-// and x a workgroup needs crosses its CU once:
+// GEMM variant (bf16), fed by DMA, in three tile shapes: MT = 256 token rows
+// by VR = 128 vocabulary rows (129 or more rows in all), MT = 128 by VR = 128
+// (65 to 128 rows), and MT = 64 by VR = 256 (at most 64 rows over a
+// vocabulary of more than two 64-row tiles per CU, where each x row then
+// serves four times as many W rows).  Every byte of W and x a workgroup needs
+// crosses its CU once:
 //   - K advances in 128-byte steps (64 elements); the W and x rows of a step go
 //     straight from memory into an LDS stage by DMA (global_load_lds, 16 bytes
 //     per lane, no registers), in a ring of S = 3 stages (48 or 40 KB): after the
@@ -585,7 +381,8 @@ __global__ __launch_bounds__(256) void lmhead_tiled_kernel(LmArgs a) {
 //   - stage rows are 128 bytes with chunk c of row r stored at chunk position
 //     c ^ ((r >> 1) & 7): a quarter-wave reading one chunk of 16 consecutive
 //     rows touches all 64 banks once;
-//   - eight waves (two per SIMD) in a WV x WT grid (VR/64 vocabulary waves):
+//   - eight waves (two per SIMD) in a WV x WT grid (VR/64 vocabulary waves;
+//     token blocks past the last row are multiplied, not stored):
 //     wave w owns vocabulary rows 64 (w % WV) .. +63 and token rows
 //     MT/WT (w / WV) .. +MT/WT-1, and issues an eighth of every step's DMA
 //     requests (at 256 x 128, four waves in a 2 x 2 grid, each with twice the
@@ -874,11 +671,11 @@ hipError_t launch_lmhead(int dtype, int mb, bool wide, const LmArgs& a, hipStrea
   const int n_vt = (a.vocab + kLmRows - 1) / kLmRows;
   const int n_grp = (n_vt + 7) / 8;
   dim3 grid(n_grp * 8 * a.n_mtiles);
-  if (mb == 8) {  // tiled variant: 65-128 token rows, 128-row vocabulary tiles (bf16)
-    if (dtype != 1) return hipErrorInvalidValue;
+  if (mb == 8) {  // GEMM variant: 128 token rows per tile, 128-row vocabulary tiles (bf16)
+    if (dtype != 1 || a.hidden_size % 256 != 0) return hipErrorInvalidValue;
     const int n_vt2 = (a.vocab + 127) / 128;
     dim3 tgrid(((n_vt2 + 7) / 8) * 8 * a.n_mtiles);
-    return launch_k(lmhead_tiled_kernel<2, 8>, tgrid, dim3(256), 0, s, nullptr, ev_stop, a);
+    return launch_k(lmhead_gemm_kernel<128, 128>, tgrid, dim3(64 * kGmWaves), 0, s, nullptr, ev_stop, a);
   }
   if (mb == 16) {  // GEMM variant: 256 token rows per tile, 128-row vocabulary tiles (bf16)
     if (dtype != 1 || a.hidden_size % 256 != 0) return hipErrorInvalidValue;

@@ -240,6 +240,22 @@ VOCAB_TIERS = [
 ]
 
 
+# 65-128 token rows take the LM head's 128 x 128 GEMM tile: two sequences of
+# 60 and 40 nodes over a vocabulary that is a multiple of neither 4 nor 128.
+@pytest.mark.timeout(300)
+def test_gemm_128_row_tile(rt):
+    vocab = 3001
+    parents = [[-1] + [(j - 1) // 3 for j in range(1, 60)], [-1] + [max(0, j - 2) for j in range(1, 40)]]
+    depth = max(8, max(_depth(p) for p in parents))
+    shp = synth.Shape("edge", "bf16", 4 * 64, 4, 2, 64, vocab, 2, 60, depth, 8)
+    # (the longest prefix goes with the largest tree: the cache holds max prefix + max nodes rows)
+    w = synth.custom(shp, parents, [260, 90], seed=241, poison_tail=True)
+    _say("[gemm 128-row tile, 100 rows] building")
+    case = workload.finish(w)
+    _say("[gemm 128-row tile, 100 rows] running GPU step")
+    compare(case, rt.run(case.w, x_out=True, tok_rank=True), "gemm 128-row tile")
+
+
 # At most 64 token rows over a vocabulary of more than two 64-row tiles per CU
 # take the LM head's 64 x 256 tile: one row (every other x row a clamped copy),
 # a partial tile and a full one, over a vocabulary that is a multiple of neither
